@@ -1,0 +1,162 @@
+/*
+ * hh.h -- C ABI of the MI355X (gfx950) decoder runtime for the "mouth" model
+ * of the Horsehair runtime path.
+ *
+ * The paper's runtime phase ends with a 1B-class decoder-only model that
+ * streams a rendered answer (Sec. 4, "Runtime phase"): one prompt evaluation,
+ * whose latency is the time to first token, followed by token-by-token
+ * streaming decode (the three speed quantities are defined in Sec. 6.2; the
+ * KV cache's memory grows with the context window, Sec. 6.6).  The paper does
+ * not describe the model's internals, so the library implements the standard
+ * Llama-style decoder: RMSNorm, rotary embeddings (rotate-half pairing), grouped
+ * query attention, SwiGLU MLP, tied or untied LM head, greedy argmax.
+ *
+ * Conventions for every call:
+ *  - Every function returns an hh_status; HH_OK is 0, errors are negative.
+ *    On any error the context's state (stream lengths, KV contents, pending
+ *    tokens, loaded weights) is unchanged and hh_last_error() describes it.
+ *  - A context is not thread-safe: use it from one host thread at a time.
+ *  - All GPU work of a context is enqueued on the HIP stream given to
+ *    hh_create.  Calls whose outputs are host memory synchronize that stream
+ *    before returning; calls whose outputs are device memory (or absent) only
+ *    enqueue.
+ *  - Pointer arguments documented "host or device" are classified with
+ *    hipPointerGetAttributes; "host" arguments must be host memory.
+ */
+#ifndef HH_H_
+#define HH_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t hh_status;
+
+enum {
+  HH_OK = 0,
+  HH_ERR_INVALID_ARG = -1,   /* bad pointer, id, size or tensor count        */
+  HH_ERR_OOM = -2,           /* arena smaller than hh_workspace_size()       */
+  HH_ERR_CONTEXT_FULL = -3,  /* a stream would exceed max_context            */
+  HH_ERR_NOT_LOADED = -4,    /* prefill/decode before hh_load_weights        */
+  HH_ERR_HIP = -5,           /* a HIP runtime call failed                    */
+  HH_ERR_UNSUPPORTED = -6    /* configuration outside what the kernels cover */
+};
+
+enum { HH_F32 = 0, HH_BF16 = 1 };                       /* weight / KV element type */
+enum { HH_LOGITS_NONE = 0, HH_LOGITS_LAST = 1, HH_LOGITS_ALL = 2 };
+
+/*
+ * Model and capacity description.  Supported: head_dim == 64, page_size == 16,
+ * n_heads a multiple of n_kv_heads with n_heads / n_kv_heads <= 8,
+ * d_model % 64 == 0, ffn_dim % 8 == 0, vocab >= 2; anything else gives
+ * HH_ERR_UNSUPPORTED.  rms_eps is added to the mean square inside the root;
+ * rope_theta is the rotary base (frequencies theta^(-2i/head_dim)).
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rms_eps, rope_theta;
+  int32_t tied_embeddings;   /* 1: LM head is the embedding matrix           */
+  int32_t dtype;             /* HH_F32 or HH_BF16: weights and KV cache      */
+  int32_t max_streams;       /* independent sequences held at once (>= 1)    */
+  int32_t max_context;       /* positions per stream (prompt + generated)    */
+  int32_t page_size;         /* KV page length in tokens; must be 16         */
+  int32_t max_prefill;       /* rows per prefill pass; 0 means max_context.
+                                Longer prompts are processed in passes.      */
+} hh_config;
+
+typedef struct hh_ctx hh_ctx;
+
+/* Bytes of device memory hh_create needs for this configuration. */
+hh_status hh_workspace_size(const hh_config* cfg, size_t* bytes);
+
+/*
+ * Create a context inside a caller-owned device arena.
+ *  arena       device pointer, 256-byte aligned, at least hh_workspace_size()
+ *              bytes; it holds weights, KV pages, RoPE tables and scratch and
+ *              must outlive hh_destroy.  The library never allocates device
+ *              memory of its own.
+ *  hip_stream  hipStream_t to enqueue on; must not be the legacy NULL stream
+ *              (decode steps are replayed as HIP graphs captured on it).
+ *  out         receives the context (host object owned by the library).
+ * Errors: INVALID_ARG (NULL/unaligned arena, NULL stream), UNSUPPORTED, OOM.
+ */
+hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void* hip_stream,
+                    hh_ctx** out);
+
+/*
+ * Copy the model weights into the arena (repacking them for the kernels).
+ *  tensors    n_tensors pointers, host or device, element type cfg.dtype
+ *             (float or bf16 bits), row-major [out, in] as in nn.Linear:
+ *               embed[vocab, d];
+ *               per layer: attn_norm[d], wq[Hq*64, d], wk[Hkv*64, d],
+ *                          wv[Hkv*64, d], wo[d, Hq*64], mlp_norm[d],
+ *                          w_gate[F, d], w_up[F, d], w_down[d, F];
+ *               final_norm[d]; lm_head[vocab, d] only if untied.
+ *  n_tensors  must be 1 + 9 * n_layers + 1 (+1 if untied).
+ * The caller may free the sources after return (the call synchronizes).
+ * Loading resets every stream.  Errors: INVALID_ARG, HIP.
+ */
+hh_status hh_load_weights(hh_ctx* ctx, const void* const* tensors, int32_t n_tensors);
+
+/*
+ * Prompt evaluation (the TTFT step): append n_tokens tokens to stream
+ * stream_id, starting at its current length, and compute the greedy next
+ * token from the last row.
+ *  tokens       host, n_tokens ids in [0, vocab).
+ *  logits_mode  HH_LOGITS_NONE, _LAST (logits = [vocab]) or _ALL
+ *               (logits = [n_tokens, vocab]); fp32, host or device.
+ *  next_token   NULL or one int32 (host or device): argmax of the last row,
+ *               lowest index among ties.  The same token is kept on the
+ *               device as the stream's pending token for hh_decode_step.
+ * Errors: INVALID_ARG (id out of range, n_tokens <= 0, NULL logits with a
+ * logits mode), CONTEXT_FULL, NOT_LOADED, HIP.
+ */
+hh_status hh_prefill(hh_ctx* ctx, int32_t stream_id, const int32_t* tokens, int32_t n_tokens,
+                     int32_t logits_mode, float* logits, int32_t* next_token);
+
+/*
+ * One greedy decode step of n_streams streams in lockstep: each listed stream
+ * consumes one token at its current length and advances by one.
+ *  stream_ids   host, n_streams distinct ids; NULL means 0..n_streams-1.
+ *  tokens       host, n_streams ids to consume (teacher forcing), or NULL to
+ *               consume each stream's pending token (the previous argmax,
+ *               kept on the device: no host round trip).
+ *  logits       NULL or [n_streams, vocab] fp32, host or device.
+ *  next_tokens  NULL or [n_streams] int32, host or device.
+ * A stream with no tokens yet decodes at position 0 (its pending token must
+ * then be given through tokens).  Errors: INVALID_ARG, CONTEXT_FULL,
+ * NOT_LOADED, HIP.
+ */
+hh_status hh_decode_step(hh_ctx* ctx, int32_t n_streams, const int32_t* stream_ids,
+                         const int32_t* tokens, float* logits, int32_t* next_tokens);
+
+/* Drop a stream's KV pages and set its length to 0 (stream_id -1: all). */
+hh_status hh_reset(hh_ctx* ctx, int32_t stream_id);
+
+/* Current length (positions held in the KV cache) of a stream. */
+hh_status hh_stream_length(const hh_ctx* ctx, int32_t stream_id, int32_t* length);
+
+/*
+ * Read back greedy outputs recorded on the device: out[i] is the argmax
+ * computed at position first_pos + i of stream_id (i.e. the prediction of the
+ * token at position first_pos + i + 1).  Positions must be < the stream's
+ * length and must have been the last row of a prefill or a decode step.
+ *  out  host, n int32.  Synchronizes the stream.
+ */
+hh_status hh_read_argmax(hh_ctx* ctx, int32_t stream_id, int32_t first_pos, int32_t n,
+                         int32_t* out);
+
+/* Destroy the host context (the arena stays the caller's). NULL is a no-op. */
+void hh_destroy(hh_ctx* ctx);
+
+/* Message of the last error on this context ("" if none); never NULL. */
+const char* hh_last_error(const hh_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HH_H_ */

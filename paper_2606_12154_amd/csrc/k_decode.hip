@@ -1,0 +1,421 @@
+// Decode-side kernels for gfx950: embedding gather, the batch-1 weight-streaming
+// GEMVs with fused prologues/epilogues (RMSNorm, RoPE + KV append, SwiGLU,
+// residual add, LM head + argmax), split-K paged GQA attention and its
+// log-sum-exp combine, row RMSNorm, and the per-step bookkeeping.
+//
+// Batch-1 decode is bound by streaming the weights from HBM once per token, so
+// every GEMV reads its matrix with coalesced 16-byte non-temporal loads (a
+// wavefront reads 1 KiB contiguous per instruction), keeps the fp32 activation
+// vector in LDS, accumulates in fp32 registers and reduces with wave64
+// shuffles.  Each workgroup owns whole output rows, so results are written
+// without atomics and are bitwise reproducible.
+#include "hh_kernels.h"
+
+namespace hh {
+
+// ---------------------------------------------------------------- step setup
+
+// Row bookkeeping + embedding gather (x[r] = E[token_r] widened to fp32).
+// Decode: row r belongs to stream row_stream[r] at position pos[stream].
+// Prefill: all rows belong to `prefill_stream`, row r at position pos + r.
+// The token is feed[r] if feed != nullptr, else the stream's pending argmax.
+template <typename TW>
+__global__ __launch_bounds__(256) void k_prep_embed(int prefill_stream, const int* __restrict__ feed,
+                                                    int* __restrict__ row_stream, int* __restrict__ row_pos,
+                                                    const int* __restrict__ pos, const int* __restrict__ pending,
+                                                    const TW* __restrict__ embed, float* __restrict__ x, int d) {
+  const int r = blockIdx.x;
+  const int s = prefill_stream >= 0 ? prefill_stream : row_stream[r];
+  const int p = pos[s] + (prefill_stream >= 0 ? r : 0);
+  const int tok = feed ? feed[r] : pending[s];
+  if (threadIdx.x == 0) {
+    row_pos[r] = p;
+    if (prefill_stream >= 0) row_stream[r] = s;
+  }
+  const TW* e = embed + (size_t)tok * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)r * d + i] = (float)e[i];
+}
+
+// Consume the argmax slots of rows [r0, r0 + n): pending token, history and
+// stream position advance to row_pos + 1.  With slot == nullptr only the
+// positions advance (an intermediate prefill pass).
+__global__ void k_finalize(int r0, int n, const int* __restrict__ row_stream, const int* __restrict__ row_pos,
+                           unsigned long long* __restrict__ slot, int* __restrict__ pending,
+                           int* __restrict__ hist, int* __restrict__ pos, int max_ctx) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int r = r0 + i;
+    const int s = row_stream[r];
+    const int p = row_pos[r];
+    if (slot) {
+      const int tok = argmax_index(slot[s]);
+      pending[s] = tok;
+      hist[(size_t)s * max_ctx + p] = tok;
+      slot[s] = 0ull;
+    }
+    pos[s] = p + 1;
+  }
+}
+
+// ---------------------------------------------------------------- GEMV core
+
+// Stage the fp32 input vector into LDS, optionally RMS-normalised:
+// xs = x * rsqrt(mean(x^2) + eps) * gain.
+__device__ __forceinline__ void stage_vector(const float* __restrict__ x, const float* __restrict__ gain,
+                                             float eps, int K, float* xs, float* red) {
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < K; i += 256) {
+    const float v = x[i];
+    xs[i] = v;
+    ss += v * v;
+  }
+  if (gain) {
+    const float tot = block_sum256(ss, red);
+    const float inv = rsqrtf(tot / (float)K + eps);
+    for (int i = threadIdx.x; i < K; i += 256) xs[i] = xs[i] * inv * gain[i];
+  }
+  __syncthreads();
+}
+
+// out[r] = dot(W[rows[r], :], xs) for R rows; rows[r] < 0 contributes 0.
+// Each thread owns 16-byte chunks c = tid, tid + 256, ... of the K axis and
+// issues all R row loads of a chunk before using them.
+template <typename TW, int R>
+__device__ __forceinline__ void gemv_rows(const TW* __restrict__ W, const int* rows, int K,
+                                          const float* xs, float* out, float* red) {
+  constexpr int V = Vec16<TW>::n;
+  const int nch = K / V;
+  float acc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r] = 0.f;
+  for (int c = threadIdx.x; c < nch; c += 256) {
+    float w[R][V];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (rows[r] >= 0) load16<TW, true>(W + (size_t)rows[r] * K + (size_t)c * V, w[r]);
+      else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) w[r][i] = 0.f;
+      }
+    }
+    float xv[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) xv[i] = xs[c * V + i];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[r] = fmaf(w[r][i], xv[i], acc[r]);
+  }
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const float s = wave_sum(acc[r]);
+    if (lane == 0) red[wv * R + r] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < R) {
+    const int r = threadIdx.x;
+    out[r] = red[r] + red[R + r] + red[2 * R + r] + red[3 * R + r];
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- GEMV kernels
+
+// Fused RMSNorm + QKV projection + RoPE + KV append for one decode row.
+// Block b handles 4 rotary pairs: pair gp = 4b + p is (head gp / 32, i = gp % 32),
+// i.e. rows head*64 + i and head*64 + i + 32 of W_qkv = [Wq; Wk; Wv].  Query
+// heads are rotated into q; key heads rotated and value heads copied into the
+// row's KV page slot.
+template <typename TW, typename TKV>
+__global__ __launch_bounds__(256) void k_qkv_gemv(const TW* __restrict__ W, const float* __restrict__ x,
+                                                  const float* __restrict__ gain, float eps, int d, int hq, int hkv,
+                                                  const int* __restrict__ row_stream, const int* __restrict__ row_pos,
+                                                  const float2* __restrict__ rope, float* __restrict__ q,
+                                                  TKV* __restrict__ kv, KvLayout L, int layer,
+                                                  const int* __restrict__ page_table) {
+  extern __shared__ float xs[];
+  __shared__ float red[4 * 8];
+  __shared__ float res[8];
+  stage_vector(x, gain, eps, d, xs, red);
+  int rows[8];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int gp = blockIdx.x * 4 + p;
+    rows[2 * p] = (gp / 32) * 64 + gp % 32;
+    rows[2 * p + 1] = rows[2 * p] + 32;
+  }
+  gemv_rows<TW, 8>(W, rows, d, xs, res, red);
+  if (threadIdx.x < 4) {
+    const int gp = blockIdx.x * 4 + threadIdx.x;
+    const int head = gp / 32, i = gp % 32;
+    const float y0 = res[2 * threadIdx.x], y1 = res[2 * threadIdx.x + 1];
+    const int s = row_stream[0], p = row_pos[0];
+    if (head < hq + hkv) {
+      const float2 cs = rope[(size_t)p * 32 + i];
+      const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+      if (head < hq) {
+        q[head * 64 + i] = r0;
+        q[head * 64 + i + 32] = r1;
+      } else {
+        const int page = page_table[(size_t)s * L.max_pages + p / kPage];
+        TKV* dst = kv + L.head_tile(layer, page, 0, head - hq) + (p % kPage) * 64;
+        dst[i] = from_f32<TKV>(r0);
+        dst[i + 32] = from_f32<TKV>(r1);
+      }
+    } else {
+      const int page = page_table[(size_t)s * L.max_pages + p / kPage];
+      TKV* dst = kv + L.head_tile(layer, page, 1, head - hq - hkv) + (p % kPage) * 64;
+      dst[i] = from_f32<TKV>(y0);
+      dst[i + 32] = from_f32<TKV>(y1);
+    }
+  }
+}
+
+// xres[row] += dot(W[row, :], in) for rows [8b, 8b + 8) < N (O and down projections).
+template <typename TW>
+__global__ __launch_bounds__(256) void k_resid_gemv(const TW* __restrict__ W, const float* __restrict__ in, int K,
+                                                    int N, float* __restrict__ xres) {
+  extern __shared__ float xs[];
+  __shared__ float red[4 * 8];
+  __shared__ float res[8];
+  stage_vector(in, nullptr, 0.f, K, xs, red);
+  int rows[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) rows[r] = blockIdx.x * 8 + r < N ? blockIdx.x * 8 + r : -1;
+  gemv_rows<TW, 8>(W, rows, K, xs, res, red);
+  if (threadIdx.x < 8 && rows[threadIdx.x] >= 0) xres[rows[threadIdx.x]] += res[threadIdx.x];
+}
+
+// Fused RMSNorm + gate/up projection + SwiGLU: m[j] = silu(Wg_j . h) * (Wu_j . h)
+// for j in [4b, 4b + 4); W = [Wg; Wu] so up row j is row F + j.
+template <typename TW>
+__global__ __launch_bounds__(256) void k_gateup_gemv(const TW* __restrict__ W, const float* __restrict__ x,
+                                                     const float* __restrict__ gain, float eps, int d, int F,
+                                                     float* __restrict__ m) {
+  extern __shared__ float xs[];
+  __shared__ float red[4 * 8];
+  __shared__ float res[8];
+  stage_vector(x, gain, eps, d, xs, red);
+  int rows[8];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int j = blockIdx.x * 4 + r;
+    rows[r] = j < F ? j : -1;
+    rows[4 + r] = j < F ? F + j : -1;
+  }
+  gemv_rows<TW, 8>(W, rows, d, xs, res, red);
+  if (threadIdx.x < 4 && rows[threadIdx.x] >= 0)
+    m[blockIdx.x * 4 + threadIdx.x] = silu(res[threadIdx.x]) * res[4 + threadIdx.x];
+}
+
+// Final RMSNorm + LM head rows [8b, 8b + 8) < V for decode row `row`:
+// optional fp32 logits, and a packed (value, index) atomicMax into the
+// stream's argmax slot (slot == nullptr: logits only).
+template <typename TW>
+__global__ __launch_bounds__(256) void k_head_gemv(const TW* __restrict__ W, const float* __restrict__ x,
+                                                   const float* __restrict__ gain, float eps, int d, int V, int row,
+                                                   const int* __restrict__ row_stream, float* __restrict__ logits,
+                                                   unsigned long long* __restrict__ slot) {
+  extern __shared__ float xs[];
+  __shared__ float red[4 * 8];
+  __shared__ float res[8];
+  stage_vector(x + (size_t)row * d, gain, eps, d, xs, red);
+  int rows[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) rows[r] = blockIdx.x * 8 + r < V ? blockIdx.x * 8 + r : -1;
+  gemv_rows<TW, 8>(W, rows, d, xs, res, red);
+  if (threadIdx.x == 0) {
+    unsigned long long best = 0ull;
+    for (int r = 0; r < 8; ++r) {
+      if (rows[r] < 0) continue;
+      if (logits) logits[rows[r]] = res[r];
+      const unsigned long long k = argmax_key(res[r], (uint32_t)rows[r]);
+      best = k > best ? k : best;
+    }
+    if (slot) atomicMax(slot + row_stream[row], best);
+  }
+}
+
+// ---------------------------------------------------------------- attention
+
+// Split count and pages per split for a row attending over t keys.
+__device__ __forceinline__ void split_plan(int t, int s_max, int& nspl, int& pps) {
+  const int npg = (t + kPage - 1) / kPage;
+  nspl = npg < s_max ? npg : s_max;
+  pps = (npg + nspl - 1) / nspl;
+  nspl = (npg + pps - 1) / pps;
+}
+
+// Paged GQA attention of row r (blockIdx.z) for kv head g (blockIdx.y), pages
+// of split blockIdx.x.  Wave w serves query heads g*G + w, g*G + w + 4, ...
+// Scores use exp2 with log2(e)/sqrt(64) folded into q; online softmax.
+// s_max > 1: writes (m, l, o[64]) partials for k_attn_combine;
+// s_max == 1: writes the normalised output directly (o32 fp32 and oM).
+template <typename TKV, typename TM>
+__global__ __launch_bounds__(256) void k_attn(const float* __restrict__ q, const TKV* __restrict__ kv, KvLayout L,
+                                              int layer, const int* __restrict__ page_table,
+                                              const int* __restrict__ row_stream, const int* __restrict__ row_pos,
+                                              int hq, int hkv, int s_max, float* __restrict__ part,
+                                              float* __restrict__ o32, TM* __restrict__ oM) {
+  const int r = blockIdx.z, g = blockIdx.y, sp = blockIdx.x;
+  const int s = row_stream[r];
+  const int t = row_pos[r] + 1;
+  int nspl, pps;
+  split_plan(t, s_max, nspl, pps);
+  if (sp >= nspl) return;
+  const int npg = (t + kPage - 1) / kPage;
+  const int pg0 = sp * pps, pg1 = min(npg, pg0 + pps);
+  const int G = hq / hkv;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int key = lane >> 2, quarter = lane & 3;
+  const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
+  for (int jj = w; jj < G; jj += 4) {
+    const int j = g * G + jj;
+    const float* qj = q + ((size_t)r * hq + j) * 64 + quarter * 16;
+    float qv[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) qv[e] = qj[e] * qscale;
+    float m = -INFINITY, l = 0.f, o = 0.f;
+    for (int pg = pg0; pg < pg1; ++pg) {
+      const int page = page_table[(size_t)s * L.max_pages + pg];
+      const TKV* Kp = kv + L.head_tile(layer, page, 0, g);
+      const TKV* Vp = kv + L.head_tile(layer, page, 1, g);
+      float kf[16];
+      load16<TKV>(Kp + key * 64 + quarter * 16, kf);
+      load16<TKV>(Kp + key * 64 + quarter * 16 + Vec16<TKV>::n, kf + Vec16<TKV>::n);
+      if constexpr (Vec16<TKV>::n == 4) {
+        load16<TKV>(Kp + key * 64 + quarter * 16 + 8, kf + 8);
+        load16<TKV>(Kp + key * 64 + quarter * 16 + 12, kf + 12);
+      }
+      float sc = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc = fmaf(qv[e], kf[e], sc);
+      sc += __shfl_xor(sc, 1, kWave);
+      sc += __shfl_xor(sc, 2, kWave);
+      if (pg * kPage + key >= t) sc = -INFINITY;
+      const float mn = fmaxf(m, wave_max(sc));
+      const float alpha = exp2f(m - mn);
+      const float p = exp2f(sc - mn);
+      l = l * alpha + wave_sum(quarter == 0 ? p : 0.f);
+      o *= alpha;
+#pragma unroll
+      for (int kk = 0; kk < kPage; ++kk) o = fmaf(__shfl(p, kk * 4, kWave), (float)Vp[kk * 64 + lane], o);
+      m = mn;
+    }
+    if (s_max == 1) {
+      const float out = o / l;
+      o32[((size_t)r * hq + j) * 64 + lane] = out;
+      if (oM) oM[((size_t)r * hq + j) * 64 + lane] = (TM)out;
+    } else {
+      float* pp = part + (((size_t)r * hq + j) * s_max + sp) * 66;
+      if (lane == 0) {
+        pp[0] = m;
+        pp[1] = l;
+      }
+      pp[2 + lane] = o;
+    }
+  }
+}
+
+// Log-sum-exp combine of the split partials of row blockIdx.y, query head
+// blockIdx.x (one lane per head dimension).
+template <typename TM>
+__global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ part,
+                                                     const int* __restrict__ row_pos, int hq, int s_max,
+                                                     float* __restrict__ o32, TM* __restrict__ oM) {
+  const int j = blockIdx.x, r = blockIdx.y, lane = threadIdx.x;
+  int nspl, pps;
+  split_plan(row_pos[r] + 1, s_max, nspl, pps);
+  const float* pp = part + ((size_t)r * hq + j) * s_max * 66;
+  float M = -INFINITY;
+  for (int i = 0; i < nspl; ++i) M = fmaxf(M, pp[i * 66]);
+  float Lsum = 0.f, O = 0.f;
+  for (int i = 0; i < nspl; ++i) {
+    const float f = exp2f(pp[i * 66] - M);
+    Lsum = fmaf(pp[i * 66 + 1], f, Lsum);
+    O = fmaf(pp[i * 66 + 2 + lane], f, O);
+  }
+  const float out = O / Lsum;
+  o32[((size_t)r * hq + j) * 64 + lane] = out;
+  if (oM) oM[((size_t)r * hq + j) * 64 + lane] = (TM)out;
+}
+
+// ---------------------------------------------------------------- rows RMSNorm
+
+// h[r] = x[r] * rsqrt(mean(x[r]^2) + eps) * gain, stored as the MFMA operand type.
+template <typename TM>
+__global__ __launch_bounds__(256) void k_rmsnorm_rows(const float* __restrict__ x, const float* __restrict__ gain,
+                                                      float eps, int d, TM* __restrict__ h) {
+  __shared__ float red[4];
+  const float* xr = x + (size_t)blockIdx.x * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) ss += xr[i] * xr[i];
+  const float inv = rsqrtf(block_sum256(ss, red) / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += 256) h[(size_t)blockIdx.x * d + i] = (TM)(xr[i] * inv * gain[i]);
+}
+
+// ---------------------------------------------------------------- launchers
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::prep_embed(hipStream_t st, int n_rows, int prefill_stream, const int* feed,
+                                            int* row_stream, int* row_pos, const int* pos, const int* pending,
+                                            const TW* embed, float* x, int d) {
+  k_prep_embed<TW><<<n_rows, 256, 0, st>>>(prefill_stream, feed, row_stream, row_pos, pos, pending, embed, x, d);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::qkv_gemv(hipStream_t st, const TW* W, const float* x, const float* gain, float eps,
+                                          int d, int hq, int hkv, const int* row_stream, const int* row_pos,
+                                          const float2* rope, float* q, TKV* kv, KvLayout L, int layer,
+                                          const int* page_table) {
+  const int blocks = (hq + 2 * hkv) * 8;  // 32 pairs per head, 4 pairs per block
+  k_qkv_gemv<TW, TKV><<<blocks, 256, d * sizeof(float), st>>>(W, x, gain, eps, d, hq, hkv, row_stream, row_pos,
+                                                               rope, q, kv, L, layer, page_table);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::resid_gemv(hipStream_t st, const TW* W, const float* in, int K, int N,
+                                            float* xres) {
+  k_resid_gemv<TW><<<(N + 7) / 8, 256, K * sizeof(float), st>>>(W, in, K, N, xres);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::gateup_gemv(hipStream_t st, const TW* W, const float* x, const float* gain,
+                                             float eps, int d, int F, float* m) {
+  k_gateup_gemv<TW><<<(F + 3) / 4, 256, d * sizeof(float), st>>>(W, x, gain, eps, d, F, m);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::head_gemv(hipStream_t st, const TW* W, const float* x, const float* gain, float eps,
+                                           int d, int V, int row, const int* row_stream, float* logits,
+                                           unsigned long long* slot) {
+  k_head_gemv<TW><<<(V + 7) / 8, 256, d * sizeof(float), st>>>(W, x, gain, eps, d, V, row, row_stream, logits, slot);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::attention(hipStream_t st, int n_rows, const float* q, const TKV* kv, KvLayout L,
+                                           int layer, const int* page_table, const int* row_stream,
+                                           const int* row_pos, int hq, int hkv, int s_max, float* part, float* o32,
+                                           TM* oM) {
+  dim3 grid(s_max, hkv, n_rows);
+  k_attn<TKV, TM><<<grid, 256, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, hkv, s_max, part, o32,
+                                        oM);
+  if (s_max > 1)
+    k_attn_combine<TM><<<dim3(hq, n_rows), 64, 0, st>>>(part, row_pos, hq, s_max, o32, oM);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::rmsnorm_rows(hipStream_t st, int n_rows, const float* x, const float* gain,
+                                              float eps, int d, TM* h) {
+  k_rmsnorm_rows<TM><<<n_rows, 256, 0, st>>>(x, gain, eps, d, h);
+}
+
+void finalize(hipStream_t st, int r0, int n, const int* row_stream, const int* row_pos, unsigned long long* slot,
+              int* pending, int* hist, int* pos, int max_ctx) {
+  k_finalize<<<1, 64, 0, st>>>(r0, n, row_stream, row_pos, slot, pending, hist, pos, max_ctx);
+}
+
+template struct DecodeKernels<float, float, float>;
+template struct DecodeKernels<__bf16, _Float16, _Float16>;
+
+}  // namespace hh

@@ -1,0 +1,46 @@
+// Load-time weight preparation kernels: widen bf16 norm gains to fp32, find
+// the largest |w| of the bf16 matrices, and repack them to fp16 times 2^s for
+// the MFMA path.  A bf16 value v with |v| * 2^s <= 2^14 converts exactly to
+// fp16 whenever |v| * 2^s >= 2^-24 (fp16 subnormals are multiples of 2^-24 and
+// a bf16 value carries 8 significant bits), so the repack is exact for every
+// weight except magnitudes below 2^-(24 + s - 7).
+#include "hh_kernels.h"
+
+namespace hh {
+
+__global__ void k_widen_bf16(const __bf16* __restrict__ src, float* __restrict__ dst, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = (float)src[i];
+}
+
+__global__ void k_absmax_bf16(const __bf16* __restrict__ src, size_t n, unsigned int* __restrict__ out) {
+  float mx = 0.f;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    mx = fmaxf(mx, fabsf((float)src[i]));
+  mx = wave_max(mx);
+  // Non-negative floats order like their bit patterns.
+  if ((threadIdx.x & 63) == 0) atomicMax(out, __float_as_uint(mx));
+}
+
+__global__ void k_bf16_to_f16_scaled(const __bf16* __restrict__ src, _Float16* __restrict__ dst, size_t n,
+                                     float scale) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = (_Float16)((float)src[i] * scale);
+}
+
+static int grid_for(size_t n) {
+  const size_t b = (n + 255) / 256;
+  return (int)(b < 4096 ? (b > 0 ? b : 1) : 4096);
+}
+
+void widen_bf16(hipStream_t st, const __bf16* src, float* dst, size_t n) {
+  k_widen_bf16<<<grid_for(n), 256, 0, st>>>(src, dst, n);
+}
+void absmax_bf16(hipStream_t st, const __bf16* src, size_t n, unsigned int* out_bits) {
+  k_absmax_bf16<<<grid_for(n), 256, 0, st>>>(src, n, out_bits);
+}
+void bf16_to_f16_scaled(hipStream_t st, const __bf16* src, _Float16* dst, size_t n, float scale) {
+  k_bf16_to_f16_scaled<<<grid_for(n), 256, 0, st>>>(src, dst, n, scale);
+}
+
+}  // namespace hh

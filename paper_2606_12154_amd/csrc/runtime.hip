@@ -1,0 +1,597 @@
+// Host runtime behind the C ABI in include/hh.h: arena carve-up, weight
+// upload and repack, per-stream KV page allocation, and the enqueue order of
+// one prefill pass / one decode step (decode steps are captured once per
+// shape into a HIP graph and replayed; positions live in device memory, so a
+// graph does not depend on where in the sequence a stream is).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "hh.h"
+#include "hh_kernels.h"
+
+using namespace hh;
+
+namespace {
+
+constexpr int kSplitMax = 64;   // attention splits per (row, kv head) in decode
+constexpr int kLogitRows = 64;  // rows of the logits staging buffer (prefill ALL)
+
+size_t al(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+  // element sizes
+  size_t ew, ekv, em;
+  int nqkv, max_pages, n_pages, rows_cap, logit_rows;
+  // byte offsets into the arena
+  size_t embed, lm_head, embedM, lm_headM;
+  std::vector<size_t> wqkv, wo, wgu, wdown, wqkvM, woM, wguM, wdownM, attn_norm, mlp_norm;
+  size_t final_norm, rope, kv, page_table, pos, pending, slot, hist;
+  size_t row_stream, row_pos, feed, x, h, q, o32, oM, m32, mM, part, logits, scratch_u32;
+  size_t total;
+};
+
+bool config_supported(const hh_config& c, std::string& why) {
+  if (c.n_layers < 0 || c.d_model <= 0 || c.n_heads <= 0 || c.n_kv_heads <= 0 || c.ffn_dim <= 0 || c.vocab < 2 ||
+      c.max_streams < 1 || c.max_context < 1 || c.max_prefill < 0) {
+    why = "non-positive dimension in config";
+    return false;
+  }
+  if (c.head_dim != 64) { why = "head_dim must be 64"; return false; }
+  if (c.page_size != kPage) { why = "page_size must be 16"; return false; }
+  if (c.n_heads % c.n_kv_heads != 0 || c.n_heads / c.n_kv_heads > 8) {
+    why = "n_heads must be a multiple of n_kv_heads, at most 8 per group";
+    return false;
+  }
+  if (c.d_model % 64 != 0) { why = "d_model must be a multiple of 64"; return false; }
+  if (c.ffn_dim % 8 != 0) { why = "ffn_dim must be a multiple of 8"; return false; }
+  if (c.d_model > 16384 || c.ffn_dim > 65536 || c.n_heads * 64 > 16384) { why = "dimension too large"; return false; }
+  if (c.dtype != HH_F32 && c.dtype != HH_BF16) { why = "dtype must be HH_F32 or HH_BF16"; return false; }
+  if (!(c.rms_eps >= 0.f) || !(c.rope_theta > 0.f)) { why = "bad rms_eps / rope_theta"; return false; }
+  return true;
+}
+
+Layout make_layout(const hh_config& c) {
+  Layout L{};
+  const bool bf = c.dtype == HH_BF16;
+  L.ew = bf ? 2 : 4;
+  L.ekv = bf ? 2 : 4;
+  L.em = bf ? 2 : 0;  // fp32 models use their weights directly as MFMA operands
+  const size_t d = c.d_model, F = c.ffn_dim, V = c.vocab, hq = c.n_heads;
+  L.nqkv = (c.n_heads + 2 * c.n_kv_heads) * 64;
+  L.max_pages = (c.max_context + kPage - 1) / kPage;
+  L.n_pages = c.max_streams * L.max_pages;
+  const int mp = c.max_prefill > 0 ? std::min(c.max_prefill, c.max_context) : c.max_context;
+  L.rows_cap = std::max(c.max_streams, mp);
+  L.logit_rows = std::max(c.max_streams, kLogitRows);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += al(bytes); return o; };
+  L.embed = take(V * d * L.ew);
+  L.lm_head = c.tied_embeddings ? L.embed : take(V * d * L.ew);
+  for (int l = 0; l < c.n_layers; ++l) {
+    L.wqkv.push_back(take((size_t)L.nqkv * d * L.ew));
+    L.wo.push_back(take(d * hq * 64 * L.ew));
+    L.wgu.push_back(take(2 * F * d * L.ew));
+    L.wdown.push_back(take(d * F * L.ew));
+  }
+  if (bf) {
+    L.embedM = take(V * d * L.em);
+    L.lm_headM = c.tied_embeddings ? L.embedM : take(V * d * L.em);
+    for (int l = 0; l < c.n_layers; ++l) {
+      L.wqkvM.push_back(take((size_t)L.nqkv * d * L.em));
+      L.woM.push_back(take(d * hq * 64 * L.em));
+      L.wguM.push_back(take(2 * F * d * L.em));
+      L.wdownM.push_back(take(d * F * L.em));
+    }
+  } else {
+    L.embedM = L.embed;
+    L.lm_headM = L.lm_head;
+    L.wqkvM = L.wqkv;
+    L.woM = L.wo;
+    L.wguM = L.wgu;
+    L.wdownM = L.wdown;
+  }
+  for (int l = 0; l < c.n_layers; ++l) {
+    L.attn_norm.push_back(take(d * 4));
+    L.mlp_norm.push_back(take(d * 4));
+  }
+  L.final_norm = take(d * 4);
+  L.rope = take((size_t)c.max_context * 32 * sizeof(float2));
+  L.kv = take((size_t)c.n_layers * L.n_pages * 2 * c.n_kv_heads * kPage * 64 * L.ekv);
+  L.page_table = take((size_t)c.max_streams * L.max_pages * 4);
+  L.pos = take((size_t)c.max_streams * 4);
+  L.pending = take((size_t)c.max_streams * 4);
+  L.slot = take((size_t)c.max_streams * 8);
+  L.hist = take((size_t)c.max_streams * c.max_context * 4);
+  const size_t R = L.rows_cap, tm = bf ? 2 : 4;
+  L.row_stream = take(R * 4);
+  L.row_pos = take(R * 4);
+  L.feed = take(R * 4);
+  L.x = take(R * d * 4);
+  L.h = take(R * std::max(d, (size_t)hq * 64) * tm);
+  L.q = take(R * hq * 64 * 4);
+  L.o32 = take(R * hq * 64 * 4);
+  L.oM = take(R * hq * 64 * tm);
+  L.m32 = take(F * 4);
+  L.mM = take(R * F * tm);
+  L.part = take((size_t)c.max_streams * hq * kSplitMax * 66 * 4);
+  L.logits = take((size_t)L.logit_rows * V * 4);
+  L.scratch_u32 = take(256);
+  L.total = off;
+  return L;
+}
+
+bool is_device_ptr(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged;
+}
+
+}  // namespace
+
+struct hh_ctx {
+  hh_config cfg{};
+  Layout L;
+  char* arena = nullptr;
+  hipStream_t stream = nullptr;
+  bool loaded = false;
+  bool use_graphs = true;
+  float wscale = 1.f;  // MFMA weights hold w * wscale (fp16 repack); epilogues multiply by 1/wscale
+  std::string err;
+  // host mirror of the device bookkeeping
+  std::vector<int> len;
+  std::vector<std::vector<int>> pages;
+  std::vector<int> free_pages;
+  std::vector<int> uploaded_streams;  // row_stream contents last uploaded for decode
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
+
+  template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(arena + off); }
+  hh_status fail(hh_status s, const std::string& m) {
+    err = m;
+    return s;
+  }
+  hh_status hip_fail(hipError_t e, const char* what) {
+    err = std::string(what) + ": " + hipGetErrorString(e);
+    return HH_ERR_HIP;
+  }
+};
+
+#define HIPCHK(ctx, expr)                                      \
+  do {                                                         \
+    hipError_t e_ = (expr);                                    \
+    if (e_ != hipSuccess) return (ctx)->hip_fail(e_, #expr);   \
+  } while (0)
+
+namespace {
+
+KvLayout kv_layout(const hh_ctx* c) { return KvLayout{c->L.n_pages, c->cfg.n_kv_heads, c->L.max_pages}; }
+
+// Enqueue the transformer layers + head for n rows whose bookkeeping
+// (row_stream, row_pos, x) has been prepared.  decode_gemv: batch-1 weight
+// streaming path; otherwise the MFMA GEMM path.  s_max: attention splits
+// (1 = direct output).  head_row >= 0: LM head + argmax of that row only;
+// head_row == -1: LM head + argmax of every row (multi-stream decode);
+// head_row == -2: no head.
+template <typename TW, typename TKV, typename TM>
+void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row, float* logits) {
+  using DK = DecodeKernels<TW, TKV, TM>;
+  using GK = GemmKernels<TM, TKV>;
+  const hh_config& g = c->cfg;
+  const Layout& L = c->L;
+  hipStream_t st = c->stream;
+  const int d = g.d_model, hq = g.n_heads, hkv = g.n_kv_heads, F = g.ffn_dim, V = g.vocab;
+  const float eps = g.rms_eps, ws = 1.f / c->wscale;
+  const KvLayout kl = kv_layout(c);
+  int* rs = c->at<int>(L.row_stream);
+  int* rp = c->at<int>(L.row_pos);
+  float* x = c->at<float>(L.x);
+  float* q = c->at<float>(L.q);
+  float* o32 = c->at<float>(L.o32);
+  TKV* kv = c->at<TKV>(L.kv);
+  const int* pt = c->at<int>(L.page_table);
+  const float2* rope = c->at<float2>(L.rope);
+  unsigned long long* slot = c->at<unsigned long long>(L.slot);
+  for (int l = 0; l < g.n_layers; ++l) {
+    const float* an = c->at<float>(L.attn_norm[l]);
+    const float* mn = c->at<float>(L.mlp_norm[l]);
+    if (decode_gemv) {
+      DK::qkv_gemv(st, c->at<TW>(L.wqkv[l]), x, an, eps, d, hq, hkv, rs, rp, rope, q, kv, kl, l, pt);
+      DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, s_max, c->at<float>(L.part), o32, nullptr);
+      DK::resid_gemv(st, c->at<TW>(L.wo[l]), o32, hq * 64, d, x);
+      DK::gateup_gemv(st, c->at<TW>(L.wgu[l]), x, mn, eps, d, F, c->at<float>(L.m32));
+      DK::resid_gemv(st, c->at<TW>(L.wdown[l]), c->at<float>(L.m32), F, d, x);
+    } else {
+      TM* h = c->at<TM>(L.h);
+      TM* oM = c->at<TM>(L.oM);
+      TM* mM = c->at<TM>(L.mM);
+      DK::rmsnorm_rows(st, n, x, an, eps, d, h);
+      GK::qkv(st, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, kv, kl, l, pt);
+      DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, s_max, c->at<float>(L.part), o32, oM);
+      GK::resid(st, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
+      DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
+      GK::gateup(st, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM);
+      GK::resid(st, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x);
+    }
+  }
+  const float* fn = c->at<float>(L.final_norm);
+  if (head_row >= 0) {
+    DK::head_gemv(st, c->at<TW>(L.lm_head), x, fn, eps, d, V, head_row, rs, logits, slot);
+  } else if (head_row == -1) {
+    if (decode_gemv) {
+      DK::head_gemv(st, c->at<TW>(L.lm_head), x, fn, eps, d, V, 0, rs, logits, slot);
+    } else {
+      TM* h = c->at<TM>(L.h);
+      DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
+      GK::logits(st, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs);
+    }
+  }
+}
+
+// One decode step for n rows (row_stream already on the device).
+template <typename TW, typename TKV, typename TM>
+void enqueue_decode(hh_ctx* c, int n, bool feed, bool want_logits) {
+  const Layout& L = c->L;
+  using DK = DecodeKernels<TW, TKV, TM>;
+  DK::prep_embed(c->stream, n, -1, feed ? c->at<int>(L.feed) : nullptr, c->at<int>(L.row_stream),
+                 c->at<int>(L.row_pos), c->at<int>(L.pos), c->at<int>(L.pending), c->at<TW>(L.embed),
+                 c->at<float>(L.x), c->cfg.d_model);
+  enqueue_layers<TW, TKV, TM>(c, n, n == 1, kSplitMax, -1, want_logits ? c->at<float>(L.logits) : nullptr);
+  finalize(c->stream, 0, n, c->at<int>(L.row_stream), c->at<int>(L.row_pos), c->at<unsigned long long>(L.slot),
+           c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos), c->cfg.max_context);
+}
+
+// Make sure stream s owns pages for positions [0, new_len); upload new entries.
+hh_status ensure_pages(hh_ctx* c, int s, int new_len) {
+  const int need = (new_len + kPage - 1) / kPage;
+  std::vector<int>& pg = c->pages[s];
+  const int first_new = (int)pg.size();
+  if (need <= first_new) return HH_OK;
+  if ((int)c->free_pages.size() < need - first_new) return c->fail(HH_ERR_CONTEXT_FULL, "KV page pool exhausted");
+  for (int i = first_new; i < need; ++i) {
+    pg.push_back(c->free_pages.back());
+    c->free_pages.pop_back();
+  }
+  int* dst = c->at<int>(c->L.page_table) + (size_t)s * c->L.max_pages + first_new;
+  HIPCHK(c, hipMemcpyAsync(dst, pg.data() + first_new, (need - first_new) * sizeof(int), hipMemcpyHostToDevice,
+                           c->stream));
+  return HH_OK;
+}
+
+template <typename TW, typename TKV, typename TM>
+hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, float* logits, int32_t* next) {
+  const Layout& L = c->L;
+  using DK = DecodeKernels<TW, TKV, TM>;
+  hipStream_t st = c->stream;
+  const int V = c->cfg.vocab;
+  hh_status rc = ensure_pages(c, s, c->len[s] + n);
+  if (rc != HH_OK) return rc;
+  const int chunk = L.rows_cap;
+  float* lbuf = c->at<float>(L.logits);
+  for (int r0 = 0; r0 < n; r0 += chunk) {
+    const int P = std::min(chunk, n - r0);
+    const bool last = r0 + P == n;
+    HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens + r0, P * sizeof(int), hipMemcpyHostToDevice, st));
+    DK::prep_embed(st, P, s, c->at<int>(L.feed), c->at<int>(L.row_stream), c->at<int>(L.row_pos), c->at<int>(L.pos),
+                   c->at<int>(L.pending), c->at<TW>(L.embed), c->at<float>(L.x), c->cfg.d_model);
+    enqueue_layers<TW, TKV, TM>(c, P, false, 1, -2, nullptr);
+    unsigned long long* slot = c->at<unsigned long long>(L.slot);
+    if (mode == HH_LOGITS_ALL) {
+      for (int b0 = 0; b0 < P; b0 += kLogitRows) {
+        const int nb = std::min(kLogitRows, P - b0);
+        for (int i = 0; i < nb; ++i)
+          DK::head_gemv(st, c->at<TW>(L.lm_head), c->at<float>(L.x), c->at<float>(L.final_norm), c->cfg.rms_eps,
+                        c->cfg.d_model, V, b0 + i, c->at<int>(L.row_stream), lbuf + (size_t)i * V,
+                        (last && b0 + i == P - 1) ? slot : nullptr);
+        HIPCHK(c, hipMemcpyAsync(logits + (size_t)(r0 + b0) * V, lbuf, (size_t)nb * V * sizeof(float),
+                                 hipMemcpyDefault, st));
+      }
+    } else if (last) {
+      DK::head_gemv(st, c->at<TW>(L.lm_head), c->at<float>(L.x), c->at<float>(L.final_norm), c->cfg.rms_eps,
+                    c->cfg.d_model, V, P - 1, c->at<int>(L.row_stream), mode == HH_LOGITS_LAST ? lbuf : nullptr,
+                    slot);
+      if (mode == HH_LOGITS_LAST)
+        HIPCHK(c, hipMemcpyAsync(logits, lbuf, (size_t)V * sizeof(float), hipMemcpyDefault, st));
+    }
+    finalize(st, P - 1, 1, c->at<int>(L.row_stream), c->at<int>(L.row_pos), last ? slot : nullptr,
+             c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos), c->cfg.max_context);
+    HIPCHK(c, hipGetLastError());
+  }
+  if (next) HIPCHK(c, hipMemcpyAsync(next, c->at<int>(L.pending) + s, sizeof(int), hipMemcpyDefault, st));
+  c->len[s] += n;
+  return HH_OK;
+}
+
+template <typename TW, typename TKV, typename TM>
+hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t* tokens, float* logits,
+                    int32_t* next) {
+  const Layout& L = c->L;
+  hipStream_t st = c->stream;
+  for (int i = 0; i < n; ++i) {
+    hh_status rc = ensure_pages(c, ids[i], c->len[ids[i]] + 1);
+    if (rc != HH_OK) return rc;
+  }
+  if (c->uploaded_streams != ids) {
+    HIPCHK(c, hipMemcpyAsync(c->at<int>(L.row_stream), ids.data(), n * sizeof(int), hipMemcpyHostToDevice, st));
+    c->uploaded_streams = ids;
+  }
+  if (tokens) HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, n * sizeof(int), hipMemcpyHostToDevice, st));
+  const bool want_logits = logits != nullptr;
+  if (c->use_graphs) {
+    auto key = std::make_tuple(n, tokens != nullptr ? 1 : 0, want_logits ? 1 : 0);
+    auto it = c->graphs.find(key);
+    if (it == c->graphs.end()) {
+      hipGraph_t graph;
+      HIPCHK(c, hipStreamBeginCapture(st, hipStreamCaptureModeRelaxed));
+      enqueue_decode<TW, TKV, TM>(c, n, tokens != nullptr, want_logits);
+      hipError_t e = hipStreamEndCapture(st, &graph);
+      if (e != hipSuccess) return c->hip_fail(e, "hipStreamEndCapture");
+      hipGraphExec_t exec;
+      e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (e != hipSuccess) return c->hip_fail(e, "hipGraphInstantiate");
+      it = c->graphs.emplace(key, exec).first;
+    }
+    HIPCHK(c, hipGraphLaunch(it->second, st));
+  } else {
+    enqueue_decode<TW, TKV, TM>(c, n, tokens != nullptr, want_logits);
+    HIPCHK(c, hipGetLastError());
+  }
+  if (logits)
+    HIPCHK(c, hipMemcpyAsync(logits, c->at<float>(L.logits), (size_t)n * c->cfg.vocab * sizeof(float),
+                             hipMemcpyDefault, st));
+  if (next) {
+    // pending[] is indexed by stream id; gather the listed streams' tokens.
+    bool contiguous = true;
+    for (int i = 0; i < n; ++i) contiguous = contiguous && ids[i] == ids[0] + i;
+    if (contiguous) {
+      HIPCHK(c, hipMemcpyAsync(next, c->at<int>(L.pending) + ids[0], n * sizeof(int), hipMemcpyDefault, st));
+    } else {
+      for (int i = 0; i < n; ++i)
+        HIPCHK(c, hipMemcpyAsync(next + i, c->at<int>(L.pending) + ids[i], sizeof(int), hipMemcpyDefault, st));
+    }
+  }
+  for (int i = 0; i < n; ++i) c->len[ids[i]] += 1;
+  return HH_OK;
+}
+
+hh_status reset_stream(hh_ctx* c, int s) {
+  for (int p : c->pages[s]) c->free_pages.push_back(p);
+  c->pages[s].clear();
+  c->len[s] = 0;
+  HIPCHK(c, hipMemsetAsync(c->at<int>(c->L.pos) + s, 0, sizeof(int), c->stream));
+  HIPCHK(c, hipMemsetAsync(c->at<int>(c->L.pending) + s, 0, sizeof(int), c->stream));
+  HIPCHK(c, hipMemsetAsync(c->at<unsigned long long>(c->L.slot) + s, 0, sizeof(unsigned long long), c->stream));
+  return HH_OK;
+}
+
+hh_status finish(hh_ctx* c, bool host_out) {
+  if (host_out) HIPCHK(c, hipStreamSynchronize(c->stream));
+  return HH_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hh_status hh_workspace_size(const hh_config* cfg, size_t* bytes) {
+  if (!cfg || !bytes) return HH_ERR_INVALID_ARG;
+  std::string why;
+  if (!config_supported(*cfg, why)) return HH_ERR_UNSUPPORTED;
+  *bytes = make_layout(*cfg).total;
+  return HH_OK;
+}
+
+hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void* hip_stream, hh_ctx** out) {
+  if (!cfg || !out || !arena || !hip_stream || (reinterpret_cast<uintptr_t>(arena) & 255)) return HH_ERR_INVALID_ARG;
+  std::string why;
+  if (!config_supported(*cfg, why)) return HH_ERR_UNSUPPORTED;
+  Layout L = make_layout(*cfg);
+  if (arena_bytes < L.total) return HH_ERR_OOM;
+  hh_ctx* c = new hh_ctx();
+  c->cfg = *cfg;
+  c->L = L;
+  c->arena = static_cast<char*>(arena);
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  const char* ge = std::getenv("HH_GRAPHS");
+  c->use_graphs = !(ge && ge[0] == '0');
+  c->len.assign(cfg->max_streams, 0);
+  c->pages.assign(cfg->max_streams, {});
+  for (int p = L.n_pages - 1; p >= 0; --p) c->free_pages.push_back(p);
+  // RoPE table: angle p * theta^(-2i/64) in fp64, cos/sin rounded to fp32.
+  std::vector<float2> rope((size_t)cfg->max_context * 32);
+  for (int p = 0; p < cfg->max_context; ++p)
+    for (int i = 0; i < 32; ++i) {
+      const double a = (double)p * std::pow((double)cfg->rope_theta, -2.0 * i / 64.0);
+      rope[(size_t)p * 32 + i] = make_float2((float)std::cos(a), (float)std::sin(a));
+    }
+  hipError_t e = hipMemcpyAsync(c->at<float2>(L.rope), rope.data(), rope.size() * sizeof(float2),
+                                hipMemcpyHostToDevice, c->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(c->arena + L.page_table, 0, L.row_stream - L.page_table, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) {
+    delete c;
+    return HH_ERR_HIP;
+  }
+  *out = c;
+  return HH_OK;
+}
+
+hh_status hh_load_weights(hh_ctx* c, const void* const* tensors, int32_t n_tensors) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  const hh_config& g = c->cfg;
+  const int expect = 1 + 9 * g.n_layers + 1 + (g.tied_embeddings ? 0 : 1);
+  if (!tensors || n_tensors != expect)
+    return c->fail(HH_ERR_INVALID_ARG, "expected " + std::to_string(expect) + " weight tensors");
+  for (int i = 0; i < n_tensors; ++i)
+    if (!tensors[i]) return c->fail(HH_ERR_INVALID_ARG, "NULL weight tensor " + std::to_string(i));
+  const Layout& L = c->L;
+  hipStream_t st = c->stream;
+  const size_t d = g.d_model, F = g.ffn_dim, V = g.vocab, hq = g.n_heads, hkv = g.n_kv_heads;
+  const bool bf = g.dtype == HH_BF16;
+  auto copy = [&](size_t off, const void* src, size_t bytes) {
+    return hipMemcpyAsync(c->arena + off, src, bytes, hipMemcpyDefault, st);
+  };
+  // Norm gains arrive in the weight dtype; they are kept as fp32.
+  char* tmp = c->arena + L.mM;  // scratch (prefill activations) while loading
+  auto gain = [&](size_t off, const void* src) {
+    if (!bf) return copy(off, src, d * 4);
+    hipError_t e = hipMemcpyAsync(tmp, src, d * 2, hipMemcpyDefault, st);
+    if (e == hipSuccess) {
+      widen_bf16(st, reinterpret_cast<const __bf16*>(tmp), c->at<float>(off), d);
+      e = hipStreamSynchronize(st);
+    }
+    return e;
+  };
+  int t = 0;
+  HIPCHK(c, copy(L.embed, tensors[t++], V * d * L.ew));
+  for (int l = 0; l < g.n_layers; ++l) {
+    HIPCHK(c, gain(L.attn_norm[l], tensors[t++]));
+    HIPCHK(c, copy(L.wqkv[l], tensors[t++], hq * 64 * d * L.ew));
+    HIPCHK(c, copy(L.wqkv[l] + hq * 64 * d * L.ew, tensors[t++], hkv * 64 * d * L.ew));
+    HIPCHK(c, copy(L.wqkv[l] + (hq + hkv) * 64 * d * L.ew, tensors[t++], hkv * 64 * d * L.ew));
+    HIPCHK(c, copy(L.wo[l], tensors[t++], d * hq * 64 * L.ew));
+    HIPCHK(c, gain(L.mlp_norm[l], tensors[t++]));
+    HIPCHK(c, copy(L.wgu[l], tensors[t++], F * d * L.ew));
+    HIPCHK(c, copy(L.wgu[l] + F * d * L.ew, tensors[t++], F * d * L.ew));
+    HIPCHK(c, copy(L.wdown[l], tensors[t++], d * F * L.ew));
+  }
+  HIPCHK(c, gain(L.final_norm, tensors[t++]));
+  if (!g.tied_embeddings) HIPCHK(c, copy(L.lm_head, tensors[t++], V * d * L.ew));
+  if (bf) {
+    // fp16 operands for the MFMA path: one power-of-two scale for all matrices.
+    std::vector<std::tuple<size_t, size_t, size_t>> list;
+    list.emplace_back(L.embed, L.embedM, V * d);
+    if (!g.tied_embeddings) list.emplace_back(L.lm_head, L.lm_headM, V * d);
+    for (int l = 0; l < g.n_layers; ++l) {
+      list.emplace_back(L.wqkv[l], L.wqkvM[l], (size_t)L.nqkv * d);
+      list.emplace_back(L.wo[l], L.woM[l], d * hq * 64);
+      list.emplace_back(L.wgu[l], L.wguM[l], 2 * F * d);
+      list.emplace_back(L.wdown[l], L.wdownM[l], d * F);
+    }
+    unsigned int* amax = c->at<unsigned int>(L.scratch_u32);
+    HIPCHK(c, hipMemsetAsync(amax, 0, 4, st));
+    for (auto& m : list) absmax_bf16(st, c->at<__bf16>(std::get<0>(m)), std::get<2>(m), amax);
+    unsigned int bits = 0;
+    HIPCHK(c, hipMemcpyAsync(&bits, amax, 4, hipMemcpyDeviceToHost, st));
+    HIPCHK(c, hipStreamSynchronize(st));
+    float mx;
+    std::memcpy(&mx, &bits, 4);
+    if (!(mx < 3.0e38f)) return c->fail(HH_ERR_INVALID_ARG, "non-finite weight");
+    const int e = mx > 0.f ? (int)std::ceil(std::log2((double)mx)) : 0;
+    const int sexp = std::max(-20, std::min(40, 14 - e));  // largest |w| * 2^s <= 2^14
+    c->wscale = std::ldexp(1.0f, sexp);
+    for (auto& m : list)
+      bf16_to_f16_scaled(st, c->at<__bf16>(std::get<0>(m)), c->at<_Float16>(std::get<1>(m)), std::get<2>(m),
+                         c->wscale);
+  } else {
+    c->wscale = 1.f;
+  }
+  HIPCHK(c, hipGetLastError());
+  HIPCHK(c, hipStreamSynchronize(st));
+  for (int s = 0; s < g.max_streams; ++s) {
+    hh_status rc = reset_stream(c, s);
+    if (rc != HH_OK) return rc;
+  }
+  HIPCHK(c, hipStreamSynchronize(st));
+  c->loaded = true;
+  c->err.clear();
+  return HH_OK;
+}
+
+hh_status hh_prefill(hh_ctx* c, int32_t s, const int32_t* tokens, int32_t n, int32_t mode, float* logits,
+                     int32_t* next) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  if (!c->loaded) return c->fail(HH_ERR_NOT_LOADED, "weights not loaded");
+  const hh_config& g = c->cfg;
+  if (s < 0 || s >= g.max_streams) return c->fail(HH_ERR_INVALID_ARG, "stream id out of range");
+  if (!tokens || n <= 0) return c->fail(HH_ERR_INVALID_ARG, "need at least one token");
+  if (mode < HH_LOGITS_NONE || mode > HH_LOGITS_ALL) return c->fail(HH_ERR_INVALID_ARG, "bad logits mode");
+  if (mode != HH_LOGITS_NONE && !logits) return c->fail(HH_ERR_INVALID_ARG, "logits buffer required");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= g.vocab) return c->fail(HH_ERR_INVALID_ARG, "token id out of range");
+  if ((long long)c->len[s] + n > g.max_context) return c->fail(HH_ERR_CONTEXT_FULL, "prompt exceeds max_context");
+  hh_status rc = g.dtype == HH_BF16 ? do_prefill<__bf16, _Float16, _Float16>(c, s, tokens, n, mode, logits, next)
+                                    : do_prefill<float, float, float>(c, s, tokens, n, mode, logits, next);
+  if (rc != HH_OK) return rc;
+  return finish(c, (logits && !is_device_ptr(logits)) || (next && !is_device_ptr(next)));
+}
+
+hh_status hh_decode_step(hh_ctx* c, int32_t n, const int32_t* stream_ids, const int32_t* tokens, float* logits,
+                         int32_t* next) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  if (!c->loaded) return c->fail(HH_ERR_NOT_LOADED, "weights not loaded");
+  const hh_config& g = c->cfg;
+  if (n < 1 || n > g.max_streams) return c->fail(HH_ERR_INVALID_ARG, "n_streams out of range");
+  std::vector<int> ids(n);
+  std::vector<char> seen(g.max_streams, 0);
+  for (int i = 0; i < n; ++i) {
+    ids[i] = stream_ids ? stream_ids[i] : i;
+    if (ids[i] < 0 || ids[i] >= g.max_streams) return c->fail(HH_ERR_INVALID_ARG, "stream id out of range");
+    if (seen[ids[i]]) return c->fail(HH_ERR_INVALID_ARG, "duplicate stream id");
+    seen[ids[i]] = 1;
+    if (c->len[ids[i]] + 1 > g.max_context) return c->fail(HH_ERR_CONTEXT_FULL, "stream at max_context");
+    if (!tokens && c->len[ids[i]] == 0) return c->fail(HH_ERR_INVALID_ARG, "empty stream needs an explicit token");
+    if (tokens && (tokens[i] < 0 || tokens[i] >= g.vocab))
+      return c->fail(HH_ERR_INVALID_ARG, "token id out of range");
+  }
+  // Page availability is checked before any state changes.
+  int need = 0;
+  for (int i = 0; i < n; ++i) {
+    const int have = (int)c->pages[ids[i]].size();
+    need += std::max(0, (c->len[ids[i]] + 1 + kPage - 1) / kPage - have);
+  }
+  if (need > (int)c->free_pages.size()) return c->fail(HH_ERR_CONTEXT_FULL, "KV page pool exhausted");
+  hh_status rc = g.dtype == HH_BF16 ? do_decode<__bf16, _Float16, _Float16>(c, n, ids, tokens, logits, next)
+                                    : do_decode<float, float, float>(c, n, ids, tokens, logits, next);
+  if (rc != HH_OK) return rc;
+  return finish(c, (logits && !is_device_ptr(logits)) || (next && !is_device_ptr(next)));
+}
+
+hh_status hh_reset(hh_ctx* c, int32_t s) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  if (s < -1 || s >= c->cfg.max_streams) return c->fail(HH_ERR_INVALID_ARG, "stream id out of range");
+  for (int i = 0; i < c->cfg.max_streams; ++i)
+    if (s == -1 || s == i) {
+      hh_status rc = reset_stream(c, i);
+      if (rc != HH_OK) return rc;
+    }
+  return HH_OK;
+}
+
+hh_status hh_stream_length(const hh_ctx* c, int32_t s, int32_t* length) {
+  if (!c || !length || s < 0 || s >= c->cfg.max_streams) return HH_ERR_INVALID_ARG;
+  *length = c->len[s];
+  return HH_OK;
+}
+
+hh_status hh_read_argmax(hh_ctx* c, int32_t s, int32_t first, int32_t n, int32_t* out) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  if (s < 0 || s >= c->cfg.max_streams || !out || n < 0 || first < 0 || first + n > c->len[s])
+    return c->fail(HH_ERR_INVALID_ARG, "argmax range outside the stream");
+  if (n == 0) return HH_OK;
+  HIPCHK(c, hipMemcpyAsync(out, c->at<int>(c->L.hist) + (size_t)s * c->cfg.max_context + first, n * sizeof(int),
+                           hipMemcpyDeviceToHost, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  return HH_OK;
+}
+
+void hh_destroy(hh_ctx* c) {
+  if (!c) return;
+  for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+  delete c;
+}
+
+const char* hh_last_error(const hh_ctx* c) { return c ? c->err.c_str() : "NULL context"; }
+
+}  // extern "C"

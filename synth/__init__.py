@@ -14,15 +14,18 @@ depends only on lengths, not on token values):
               vocab 128256, eps 1e-5, RoPE theta 5e5, tied, bf16.
 
 Weight recipe: every matrix is i.i.d. N(0, 0.02^2), drawn in fp32 with
-``numpy.random.Generator(PCG64(seed)).standard_normal`` in the tensor order of
-the C ABI; bf16 models round each fp32 draw to nearest-even bf16.  RMSNorm
-gains are 1.0 unless ``gain_std`` > 0, in which case they are 1 + N(0,
-gain_std^2) from a second generator (seed + 7919) so the matrices are the same
-either way.
+``numpy.random.Generator(PCG64(SeedSequence([seed, i]))).standard_normal``
+where i is the tensor's index in the C-ABI load order (one generator per
+tensor, so tensors can be drawn in parallel); bf16 models round each fp32 draw
+to nearest-even bf16.  RMSNorm gains are 1.0 unless ``gain_std`` > 0, in which
+case they are 1 + N(0, gain_std^2) from the generator of
+SeedSequence([seed, i, 1]), so the matrices are the same either way.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
+import os
 from typing import Dict, List
 
 import numpy as np
@@ -105,25 +108,30 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
+def _draw_tensor(shape: "ModelShape", seed: int, i: int, shp, gain_std: float) -> np.ndarray:
+    if len(shp) == 1:
+        if gain_std > 0:
+            g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, i, 1])))
+            w = (1.0 + gain_std * g.standard_normal(shp)).astype(np.float32)
+        else:
+            w = np.ones(shp, dtype=np.float32)
+    else:
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, i])))
+        w = g.standard_normal(shp, dtype=np.float32)
+        w *= np.float32(0.02)
+    return f32_to_bf16_bits(w) if shape.dtype == BF16 else w
+
+
 def make_weights(shape: ModelShape, seed: int, gain_std: float = 0.0) -> List[np.ndarray]:
     """Seeded weights in C-ABI tensor order and storage format.
 
     fp32 models give float32 arrays; bf16 models give uint16 arrays of bf16
     bits.  Matrices are N(0, 0.02^2); gains are ones (or 1 + N(0, gain_std^2))."""
-    rng = np.random.Generator(np.random.PCG64(seed))
-    grng = np.random.Generator(np.random.PCG64(seed + 7919))
-    out = []
-    for name, shp in shape.tensor_specs():
-        if len(shp) == 1:
-            if gain_std > 0:
-                w = (1.0 + gain_std * grng.standard_normal(shp)).astype(np.float32)
-            else:
-                w = np.ones(shp, dtype=np.float32)
-        else:
-            w = rng.standard_normal(shp, dtype=np.float32)
-            w *= np.float32(0.02)
-        out.append(f32_to_bf16_bits(w) if shape.dtype == BF16 else w)
-    return out
+    specs = shape.tensor_specs()
+    workers = max(1, min(16, os.cpu_count() or 1))
+    with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+        futs = [ex.submit(_draw_tensor, shape, seed, i, shp, gain_std) for i, (_, shp) in enumerate(specs)]
+        return [f.result() for f in futs]
 
 
 def weights_as_f64(shape: ModelShape, tensors: List[np.ndarray]) -> Dict[str, np.ndarray]:

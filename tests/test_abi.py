@@ -1,0 +1,62 @@
+"""C-ABI surface: the library loads, exports every function include/hh.h
+declares, and rejects bad configurations without touching a GPU (CPU only)."""
+import os
+import re
+
+import pytest
+
+import synth
+from paper_2606_12154_amd import hh
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "hh.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hh_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_names():
+    assert declared_functions() == sorted(hh.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = hh.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_workspace_sizes():
+    tiny = hh.hh_workspace_size(hh.make_config(synth.TINY, 4, 256))
+    assert 10_000_000 < tiny < 100_000_000
+    big = hh.hh_workspace_size(hh.make_config(synth.ONE_B, 1, 8704, 8192))
+    # bf16 weights + fp16 MFMA copy (2 x 2.47 GB) + fp16 KV (32 KiB/token) + scratch
+    assert 2 * 2_471_632_896 + 8704 * 32768 < big < 7_000_000_000
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 128, hh.HH_ERR_UNSUPPORTED),
+    ("page_size", 32, hh.HH_ERR_UNSUPPORTED),
+    ("n_kv_heads", 3, hh.HH_ERR_UNSUPPORTED),
+    ("d_model", 200, hh.HH_ERR_UNSUPPORTED),
+    ("ffn_dim", 690, hh.HH_ERR_UNSUPPORTED),
+    ("dtype", 7, hh.HH_ERR_UNSUPPORTED),
+    ("max_streams", 0, hh.HH_ERR_UNSUPPORTED),
+])
+def test_unsupported_configs(field, value, status):
+    cfg = hh.make_config(synth.TINY, 2, 128)
+    setattr(cfg, field, value)
+    with pytest.raises(hh.HHError) as e:
+        hh.hh_workspace_size(cfg)
+    assert e.value.status == status
+
+
+def test_create_rejects_null_arena_and_small_arena():
+    cfg = hh.make_config(synth.TINY, 2, 128)
+    with pytest.raises(hh.HHError) as e:
+        hh.hh_create(cfg, 0, 1 << 30, 1)
+    assert e.value.status == hh.HH_ERR_INVALID_ARG
+    with pytest.raises(hh.HHError) as e:
+        hh.hh_create(cfg, 1 << 20, 16, 1)
+    assert e.value.status == hh.HH_ERR_OOM
