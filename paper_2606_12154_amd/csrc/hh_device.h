@@ -50,6 +50,41 @@ __device__ __forceinline__ void load16(const T* p, float* f) {
 
 template <typename T> __device__ __forceinline__ T from_f32(float x) { return (T)x; }
 
+// DPP lane moves (VALU, no LDS round trip).  CTRL: 0xB1 quad_perm [1,0,3,2]
+// (partner lane ^ 1), 0x4E quad_perm [2,3,0,1] (lane ^ 2), 0x120 + n row_ror:n
+// (rotate right by n within each row of 16 lanes).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_read(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+// Sum / max over the 16 lanes of each row (every lane of the row gets it).
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x124>(v);
+  v += dpp<0x128>(v);
+  return v;
+}
+__device__ __forceinline__ float row_max16(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x124>(v));
+  v = fmaxf(v, dpp<0x128>(v));
+  return v;
+}
+// Wave-wide sum / max, returned uniformly (row totals combined by readlane).
+__device__ __forceinline__ float wave_sum_u(float v) {
+  v = row_sum16(v);
+  return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
+}
+__device__ __forceinline__ float wave_max_u(float v) {
+  v = row_max16(v);
+  return fmaxf(fmaxf(lane_read(v, 0), lane_read(v, 16)), fmaxf(lane_read(v, 32), lane_read(v, 48)));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

@@ -40,6 +40,62 @@ struct GemmKernels {
                      unsigned long long* slot, const int* row_stream);
 };
 
+// ---- batch-1 decode step as one persistent kernel (k_step.hip)
+constexpr int kStepThreads = 512;     // threads per workgroup (8 waves)
+constexpr int kStepResFloats = 1024;  // LDS row results per workgroup and phase
+constexpr int kStepMaxLayers = 63;    // layers the persistent kernel supports
+constexpr int kStepMaxItemPages = 2048;  // KV pages of one attention item (32768 positions)
+
+template <typename TW>
+struct LayerPtrs {
+  const TW* wqkv;   // [(Hq + 2 Hkv) * 64, d]
+  const TW* wo;     // [d, Hq * 64]
+  const TW* wgu;    // [2F, d] = [Wgate; Wup]
+  const TW* wdown;  // [d, F]
+  const float* attn_norm;
+  const float* mlp_norm;
+};
+
+template <typename TW, typename TKV>
+struct StepParams {
+  int d, F, hq, hkv, V, n_layers, max_ctx, stream, stage_floats;
+  float eps;
+  unsigned epoch;              // base epoch of this step (distinct for every step)
+  const LayerPtrs<TW>* layer;  // device array [n_layers]
+  const TW* embed;
+  const TW* head;
+  const float* final_norm;
+  const float2* rope;
+  TKV* kvc;
+  KvLayout kv;
+  const int* page_table;
+  int* pos;
+  int* pending;
+  int* hist;
+  const int* feed;  // nullptr: consume the pending token
+  float* logits;    // nullptr or [V]
+  // Epoch-tagged exchange words (fp32 bits | epoch << 32) between workgroups.
+  unsigned long long* ll_xa;    // [d] x after the O projection
+  unsigned long long* ll_xb;    // [d] x after the down projection
+  unsigned long long* ll_q;     // [Hq * 64] rotated queries
+  unsigned long long* ll_kn;    // [Hkv * 64] rotated key of the current position
+  unsigned long long* ll_vn;    // [Hkv * 64] value of the current position
+  unsigned long long* ll_part;  // [Hq][nwg / Hkv][66] attention split partials
+  unsigned long long* ll_o;     // [Hq * 64] attention output
+  unsigned long long* ll_m;     // [F] SwiGLU output
+  unsigned long long* ll_keys;  // [2 * nwg] per-workgroup argmax keys
+  int* err;                     // set to 1 if a wait timed out
+  unsigned long long* trace;    // nullptr, or [nwg][n_layers + 1][32] phase timestamps
+};
+
+template <typename TW, typename TKV>
+struct StepKernel {
+  static bool supports(int d, int F, int hq, int hkv, int V, int n_layers, int nwg);
+  static hipError_t launch(const StepParams<TW, TKV>& P, int nwg, hipStream_t st);
+  static int max_blocks_per_cu(int d, int F, int hq);
+  static size_t lds_bytes(int d, int F, int hq);
+};
+
 // Load-time weight preparation.
 void widen_bf16(hipStream_t st, const __bf16* src, float* dst, size_t n);
 void absmax_bf16(hipStream_t st, const __bf16* src, size_t n, unsigned int* out_bits);

@@ -24,6 +24,7 @@ namespace {
 
 constexpr int kSplitMax = 64;   // attention splits per (row, kv head) in decode
 constexpr int kLogitRows = 64;  // rows of the logits staging buffer (prefill ALL)
+constexpr int kMaxStepWG = 1024; // upper bound on persistent decode-step workgroups
 
 size_t al(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -34,7 +35,7 @@ struct Layout {
   // byte offsets into the arena
   size_t embed, lm_head, embedM, lm_headM;
   std::vector<size_t> wqkv, wo, wgu, wdown, wqkvM, woM, wguM, wdownM, attn_norm, mlp_norm;
-  size_t final_norm, rope, kv, page_table, pos, pending, slot, hist;
+  size_t final_norm, rope, kv, page_table, pos, pending, slot, hist, ll, ll_words, layer_tab, trace;
   size_t row_stream, row_pos, feed, x, h, q, o32, oM, m32, mM, part, logits, scratch_u32;
   size_t total;
 };
@@ -111,6 +112,14 @@ Layout make_layout(const hh_config& c) {
   L.pending = take((size_t)c.max_streams * 4);
   L.slot = take((size_t)c.max_streams * 8);
   L.hist = take((size_t)c.max_streams * c.max_context * 4);
+  // Epoch-tagged exchange words of the persistent decode kernel (see k_step.hip):
+  // xa, xb [d], q [Hq*64], kn, vn [Hkv*64], partials [Hq][kMaxStepWG][66],
+  // o [Hq*64], m [F], keys [2*kMaxStepWG], then the error flag.
+  L.ll_words = 2 * d + 2 * (size_t)hq * 64 + 2 * (size_t)c.n_kv_heads * 64 + (size_t)hq * kMaxStepWG * 66 + F +
+               2 * kMaxStepWG + 8;
+  L.ll = take(L.ll_words * 8);
+  L.layer_tab = take((size_t)c.n_layers * sizeof(LayerPtrs<float>));
+  L.trace = take((size_t)kMaxStepWG * (c.n_layers + 1) * 32 * 8);  // optional phase timestamps
   const size_t R = L.rows_cap, tm = bf ? 2 : 4;
   L.row_stream = take(R * 4);
   L.row_pos = take(R * 4);
@@ -148,6 +157,9 @@ struct hh_ctx {
   bool loaded = false;
   bool use_graphs = true;
   float wscale = 1.f;  // MFMA weights hold w * wscale (fp16 repack); epilogues multiply by 1/wscale
+  int step_wg = 0;     // workgroups of the persistent batch-1 decode kernel (0: not usable)
+  unsigned step_count = 0;  // persistent-kernel launches so far (names each step's epochs)
+  std::string trace_path;   // HH_STEP_TRACE: file receiving the last traced step's phase timestamps
   std::string err;
   // host mirror of the device bookkeeping
   std::vector<int> len;
@@ -251,6 +263,97 @@ void enqueue_decode(hh_ctx* c, int n, bool feed, bool want_logits) {
            c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos), c->cfg.max_context);
 }
 
+// Size the persistent decode kernel to one workgroup per CU (all co-resident)
+// and upload the per-layer weight pointer table it reads.
+template <typename TW>
+hipError_t setup_step_tables(hh_ctx* c) {
+  const hh_config& g = c->cfg;
+  const Layout& L = c->L;
+  std::vector<LayerPtrs<TW>> tab(g.n_layers);
+  for (int l = 0; l < g.n_layers; ++l)
+    tab[l] = LayerPtrs<TW>{c->at<TW>(L.wqkv[l]), c->at<TW>(L.wo[l]), c->at<TW>(L.wgu[l]), c->at<TW>(L.wdown[l]),
+                           c->at<float>(L.attn_norm[l]), c->at<float>(L.mlp_norm[l])};
+  if (g.n_layers == 0) return hipSuccess;
+  hipError_t e = hipMemcpyAsync(c->arena + L.layer_tab, tab.data(), tab.size() * sizeof(LayerPtrs<TW>),
+                                hipMemcpyHostToDevice, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  return e;
+}
+
+template <typename TW, typename TKV>
+int step_workgroups(const hh_config& g) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  const char* env = std::getenv("HH_STEP_KERNEL");
+  if (env && env[0] == '0') return 0;
+  const int nwg = std::min(cus, kMaxStepWG);
+  if (!StepKernel<TW, TKV>::supports(g.d_model, g.ffn_dim, g.n_heads, g.n_kv_heads, g.vocab, g.n_layers, nwg))
+    return 0;
+  if ((g.max_context + kPage - 1) / kPage > kStepMaxItemPages) return 0;
+  if (StepKernel<TW, TKV>::max_blocks_per_cu(g.d_model, g.ffn_dim, g.n_heads) < 1) return 0;
+  return nwg;
+}
+
+hipError_t setup_step_kernel(hh_ctx* c) {
+  if (c->cfg.dtype == HH_BF16) {
+    c->step_wg = step_workgroups<__bf16, _Float16>(c->cfg);
+    return setup_step_tables<__bf16>(c);
+  }
+  c->step_wg = step_workgroups<float, float>(c->cfg);
+  return setup_step_tables<float>(c);
+}
+
+template <typename TW, typename TKV>
+hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
+  const hh_config& g = c->cfg;
+  const Layout& L = c->L;
+  StepParams<TW, TKV> P{};
+  P.d = g.d_model;
+  P.F = g.ffn_dim;
+  P.hq = g.n_heads;
+  P.hkv = g.n_kv_heads;
+  P.V = g.vocab;
+  P.n_layers = g.n_layers;
+  P.max_ctx = g.max_context;
+  P.stream = s;
+  P.stage_floats = std::max(std::max(g.d_model, g.ffn_dim), g.n_heads * 64);
+  P.eps = g.rms_eps;
+  // Each step owns 512 epochs (8 phases x 64 layers); epoch 0 is never used,
+  // so the zero-initialised exchange words never look current.
+  c->step_count += 1;
+  P.epoch = c->step_count * 512u;
+  P.layer = c->at<LayerPtrs<TW>>(L.layer_tab);
+  P.embed = c->at<TW>(L.embed);
+  P.head = c->at<TW>(L.lm_head);
+  P.final_norm = c->at<float>(L.final_norm);
+  P.rope = c->at<float2>(L.rope);
+  P.kvc = c->at<TKV>(L.kv);
+  P.kv = kv_layout(c);
+  P.page_table = c->at<int>(L.page_table);
+  P.pos = c->at<int>(L.pos);
+  P.pending = c->at<int>(L.pending);
+  P.hist = c->at<int>(L.hist);
+  P.feed = feed ? c->at<int>(L.feed) : nullptr;
+  P.logits = want_logits ? c->at<float>(L.logits) : nullptr;
+  unsigned long long* w = c->at<unsigned long long>(L.ll);
+  const size_t d = g.d_model, hq = g.n_heads, hkv = g.n_kv_heads;
+  P.ll_xa = w;
+  P.ll_xb = P.ll_xa + d;
+  P.ll_q = P.ll_xb + d;
+  P.ll_kn = P.ll_q + hq * 64;
+  P.ll_vn = P.ll_kn + hkv * 64;
+  P.ll_part = P.ll_vn + hkv * 64;
+  P.ll_o = P.ll_part + hq * kMaxStepWG * 66;
+  P.ll_m = P.ll_o + hq * 64;
+  P.ll_keys = P.ll_m + g.ffn_dim;
+  P.err = reinterpret_cast<int*>(P.ll_keys + 2 * kMaxStepWG);
+  P.trace = c->trace_path.empty() ? nullptr : c->at<unsigned long long>(L.trace);
+  const hipError_t e = StepKernel<TW, TKV>::launch(P, c->step_wg, c->stream);
+  if (e != hipSuccess) return c->hip_fail(e, "decode-step kernel launch");
+  return HH_OK;
+}
+
 // Make sure stream s owns pages for positions [0, new_len); upload new entries.
 hh_status ensure_pages(hh_ctx* c, int s, int new_len) {
   const int need = (new_len + kPage - 1) / kPage;
@@ -327,7 +430,10 @@ hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t
   }
   if (tokens) HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, n * sizeof(int), hipMemcpyHostToDevice, st));
   const bool want_logits = logits != nullptr;
-  if (c->use_graphs) {
+  if (n == 1 && c->step_wg > 0) {
+    hh_status rc = launch_step<TW, TKV>(c, ids[0], tokens != nullptr, want_logits);
+    if (rc != HH_OK) return rc;
+  } else if (c->use_graphs) {
     auto key = std::make_tuple(n, tokens != nullptr ? 1 : 0, want_logits ? 1 : 0);
     auto it = c->graphs.find(key);
     if (it == c->graphs.end()) {
@@ -375,8 +481,16 @@ hh_status reset_stream(hh_ctx* c, int s) {
   return HH_OK;
 }
 
+// Synchronize when outputs live in host memory; report a timed-out grid
+// barrier of the persistent decode kernel at that point.
 hh_status finish(hh_ctx* c, bool host_out) {
-  if (host_out) HIPCHK(c, hipStreamSynchronize(c->stream));
+  if (!host_out) return HH_OK;
+  int err = 0;
+  if (c->step_wg > 0)
+    HIPCHK(c, hipMemcpyAsync(&err, c->at<unsigned long long>(c->L.ll) + c->L.ll_words - 8, sizeof(int),
+                             hipMemcpyDeviceToHost, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  if (err) return c->fail(HH_ERR_HIP, "decode-step exchange wait timed out (workgroups not co-resident)");
   return HH_OK;
 }
 
@@ -403,6 +517,8 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   c->L = L;
   c->arena = static_cast<char*>(arena);
   c->stream = static_cast<hipStream_t>(hip_stream);
+  const char* tp = std::getenv("HH_STEP_TRACE");
+  if (tp) c->trace_path = tp;
   const char* ge = std::getenv("HH_GRAPHS");
   c->use_graphs = !(ge && ge[0] == '0');
   c->len.assign(cfg->max_streams, 0);
@@ -418,6 +534,7 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   hipError_t e = hipMemcpyAsync(c->at<float2>(L.rope), rope.data(), rope.size() * sizeof(float2),
                                 hipMemcpyHostToDevice, c->stream);
   if (e == hipSuccess) e = hipMemsetAsync(c->arena + L.page_table, 0, L.row_stream - L.page_table, c->stream);
+  if (e == hipSuccess) e = setup_step_kernel(c);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) {
     delete c;
@@ -588,6 +705,19 @@ hh_status hh_read_argmax(hh_ctx* c, int32_t s, int32_t first, int32_t n, int32_t
 
 void hh_destroy(hh_ctx* c) {
   if (!c) return;
+  if (!c->trace_path.empty() && c->step_wg > 0 && c->step_count > 0) {
+    // Diagnostic dump: binary [nwg][n_layers + 1][32] uint64 timestamps of the last step.
+    const size_t n = (size_t)c->step_wg * (c->cfg.n_layers + 1) * 32;
+    std::vector<unsigned long long> h(n);
+    if (hipMemcpyAsync(h.data(), c->at<unsigned long long>(c->L.trace), n * 8, hipMemcpyDeviceToHost, c->stream) ==
+            hipSuccess &&
+        hipStreamSynchronize(c->stream) == hipSuccess) {
+      if (FILE* f = std::fopen(c->trace_path.c_str(), "wb")) {
+        std::fwrite(h.data(), 8, n, f);
+        std::fclose(f);
+      }
+    }
+  }
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
   delete c;
 }
