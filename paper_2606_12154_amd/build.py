@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libhh.so")
 BUILD = os.path.join(ROOT, "_build")
-SOURCES = ["k_decode.hip", "k_gemm.hip", "k_load.hip", "k_step.hip", "runtime.hip"]
+SOURCES = ["k_decode.hip", "k_gemm.hip", "k_attn_prefill.hip", "k_load.hip", "k_step.hip", "runtime.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -29,16 +29,28 @@ struct DecodeKernels {
 void finalize(hipStream_t st, int r0, int n, const int* row_stream, const int* row_pos, unsigned long long* slot,
               int* pending, int* hist, int* pos, int max_ctx);
 
+// fp32 scratch (in the context's arena) for split-K partial tiles of the
+// MFMA GEMM; splits are reduced until the partials fit.
+struct GemmWorkspace {
+  float* ptr;
+  size_t bytes;
+};
+
 template <typename TM, typename TKV>
 struct GemmKernels {
-  static void qkv(hipStream_t st, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
-                  const int* row_stream, const int* row_pos, const float2* rope, float* q, TKV* kv, KvLayout L,
-                  int layer, const int* page_table);
-  static void resid(hipStream_t st, const TM* A, int M, const TM* W, int K, int N, float scale, float* x);
-  static void gateup(hipStream_t st, const TM* A, int M, const TM* W, int d, int F, float scale, TM* m);
-  static void logits(hipStream_t st, const TM* A, int M, const TM* W, int d, int V, float scale, float* logits,
+  static void qkv(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
+                  const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM, TKV* kv,
+                  KvLayout L, int layer, const int* page_table);
+  static void resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x);
+  static void gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale, TM* m);
+  static void logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale, float* logits,
                      unsigned long long* slot, const int* row_stream);
 };
+
+// ---- causal flash attention for prefill rows of one stream (k_attn_prefill.hip)
+bool flash_prefill_supported(int G);
+void flash_prefill(hipStream_t st, const _Float16* qM, const _Float16* kv, KvLayout L, int layer,
+                   const int* page_table, int s, int p0, int n_rows, int hq, int hkv, _Float16* oM);
 
 // ---- batch-1 decode step as one persistent kernel (k_step.hip)
 constexpr int kStepThreads = 512;     // threads per workgroup (8 waves)

@@ -5,22 +5,24 @@
 // Operands are of type TM: _Float16 for bf16 models (the bf16 weights are
 // repacked at load time to fp16 times a power-of-two scale, exact for this
 // weight range, and activations are rounded to fp16 once), float for fp32
-// models (v_mfma_f32_16x16x4_f32).  A 256-thread block computes a 64x64 tile:
-// four waves in a 2x2 arrangement each own a 32x32 quarter as 2x2 MFMA 16x16
-// fragments; K advances in steps of 32 through LDS.  The finished tile is
-// staged in LDS so the epilogue can use any column pairing (rotary pairs
-// i / i + 32 of a head, gate / up columns) without shuffles.
+// models (v_mfma_f32_16x16x4_f32).  The finished tile is staged in LDS so the
+// epilogue can use any column pairing (rotary pairs i / i + 32 of a head,
+// gate / up columns) without shuffles.
 #include "hh_kernels.h"
+
+#include <algorithm>
 
 namespace hh {
 
-constexpr int GBM = 64, GBN = 64, GBK = 32;
-constexpr int GLDC = GBN + 4;
-
 // ---------------------------------------------------------------- epilogues
+//
+// The GEMM works on logical columns n; epi.b_row(n) names the weight row of
+// column n (-1: none).  A tile covers logical columns [n0, n0 + BN) and the
+// epilogue receives the finished fp32 tile Cs[BM][ldc] in LDS.
 
-// Columns of W for tile nt: head nt of [Wq; Wk; Wv] (64 rows).  Rotates query
-// heads into q and key heads into the KV page slot of each row; copies values.
+// Columns = rows of [Wq; Wk; Wv]; a tile holds whole heads (BN % 64 == 0).
+// Rotates query heads into q (and qM), key heads into the KV page slot of
+// each row; copies value heads.
 template <typename TKV>
 struct EpiQKV {
   int hq, hkv;
@@ -29,17 +31,19 @@ struct EpiQKV {
   const int* row_pos;
   const float2* rope;
   float* q;
+  TKV* qM;  // nullptr, or rotated queries again in the MFMA operand type
   TKV* kv;
   KvLayout L;
   int layer;
   const int* page_table;
-  __device__ int b_row(int nt, int c) const { return nt * 64 + c; }
-  __device__ void operator()(const float* Cs, int m0, int M, int nt) const {
-    const int head = nt;
-    for (int idx = threadIdx.x; idx < GBM * 32; idx += 256) {
-      const int r = idx >> 5, i = idx & 31, row = m0 + r;
-      if (row >= M) continue;
-      const float y0 = Cs[r * GLDC + i] * scale, y1 = Cs[r * GLDC + i + 32] * scale;
+  __device__ int b_row(int n) const { return n < (hq + 2 * hkv) * 64 ? n : -1; }
+  __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
+    const int nh = BN / 64;
+    for (int idx = threadIdx.x; idx < BM * 32 * nh; idx += blockDim.x) {
+      const int r = idx / (32 * nh), hh = (idx / 32) % nh, i = idx & 31, row = m0 + r;
+      const int head = n0 / 64 + hh;
+      if (row >= M || head >= hq + 2 * hkv) continue;
+      const float y0 = Cs[r * ldc + hh * 64 + i] * scale, y1 = Cs[r * ldc + hh * 64 + i + 32] * scale;
       const int s = row_stream[row], p = row_pos[row];
       if (head < hq + hkv) {
         const float2 cs = rope[(size_t)p * 32 + i];
@@ -47,6 +51,10 @@ struct EpiQKV {
         if (head < hq) {
           q[((size_t)row * hq + head) * 64 + i] = r0;
           q[((size_t)row * hq + head) * 64 + i + 32] = r1;
+          if (qM) {
+            qM[((size_t)row * hq + head) * 64 + i] = (TKV)r0;
+            qM[((size_t)row * hq + head) * 64 + i + 32] = (TKV)r1;
+          }
         } else {
           const int page = page_table[(size_t)s * L.max_pages + p / kPage];
           TKV* dst = kv + L.head_tile(layer, page, 0, head - hq) + (p % kPage) * 64;
@@ -68,31 +76,33 @@ struct EpiResid {
   int N;
   float scale;
   float* x;
-  __device__ int b_row(int nt, int c) const { return nt * 64 + c < N ? nt * 64 + c : -1; }
-  __device__ void operator()(const float* Cs, int m0, int M, int nt) const {
-    for (int idx = threadIdx.x; idx < GBM * GBN; idx += 256) {
-      const int r = idx >> 6, c = idx & 63, row = m0 + r, col = nt * 64 + c;
-      if (row < M && col < N) x[(size_t)row * N + col] += Cs[r * GLDC + c] * scale;
+  __device__ int b_row(int n) const { return n < N ? n : -1; }
+  __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
+    for (int idx = threadIdx.x; idx < BM * BN; idx += blockDim.x) {
+      const int r = idx / BN, c = idx % BN, row = m0 + r, col = n0 + c;
+      if (row < M && col < N) x[(size_t)row * N + col] += Cs[r * ldc + c] * scale;
     }
   }
 };
 
-// Tile nt covers gate columns [32nt, 32nt + 32) and the matching up columns
-// (rows F + j of [Wg; Wu]); m[row, j] = silu(gate) * up.
+// A tile of width BN holds gate columns j = tile * BN/2 + c (c < BN/2) and,
+// in its second half, the matching up columns (rows F + j of [Wg; Wu]);
+// m[row, j] = silu(gate) * up.
 template <typename TM>
 struct EpiGateUp {
-  int F;
+  int F, half;
   float scale;
   TM* m;
-  __device__ int b_row(int nt, int c) const {
-    const int j = nt * 32 + (c & 31);
-    return j < F ? (c < 32 ? j : F + j) : -1;
+  __device__ int b_row(int n) const {
+    const int c = n % (2 * half), j = (n / (2 * half)) * half + (c < half ? c : c - half);
+    return j < F ? (c < half ? j : F + j) : -1;
   }
-  __device__ void operator()(const float* Cs, int m0, int M, int nt) const {
-    for (int idx = threadIdx.x; idx < GBM * 32; idx += 256) {
-      const int r = idx >> 5, j = idx & 31, row = m0 + r, col = nt * 32 + j;
+  __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
+    const int j0 = (n0 / BN) * half;
+    for (int idx = threadIdx.x; idx < BM * half; idx += blockDim.x) {
+      const int r = idx / half, c = idx % half, row = m0 + r, col = j0 + c;
       if (row >= M || col >= F) continue;
-      const float g = Cs[r * GLDC + j] * scale, u = Cs[r * GLDC + 32 + j] * scale;
+      const float g = Cs[r * ldc + c] * scale, u = Cs[r * ldc + half + c] * scale;
       m[(size_t)row * F + col] = (TM)(silu(g) * u);
     }
   }
@@ -106,18 +116,18 @@ struct EpiLogits {
   float* logits;
   unsigned long long* slot;
   const int* row_stream;
-  __device__ int b_row(int nt, int c) const { return nt * 64 + c < V ? nt * 64 + c : -1; }
-  __device__ void operator()(const float* Cs, int m0, int M, int nt) const {
+  __device__ int b_row(int n) const { return n < V ? n : -1; }
+  __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     if (logits)
-      for (int idx = threadIdx.x; idx < GBM * GBN; idx += 256) {
-        const int r = idx >> 6, c = idx & 63, row = m0 + r, col = nt * 64 + c;
-        if (row < M && col < V) logits[(size_t)row * V + col] = Cs[r * GLDC + c] * scale;
+      for (int idx = threadIdx.x; idx < BM * BN; idx += blockDim.x) {
+        const int r = idx / BN, c = idx % BN, row = m0 + r, col = n0 + c;
+        if (row < M && col < V) logits[(size_t)row * V + col] = Cs[r * ldc + c] * scale;
       }
-    if (slot && threadIdx.x < GBM && m0 + threadIdx.x < M) {
+    if (slot && (int)threadIdx.x < BM && m0 + (int)threadIdx.x < M) {
       const int r = threadIdx.x;
       unsigned long long best = 0ull;
-      for (int c = 0; c < GBN && nt * 64 + c < V; ++c) {
-        const unsigned long long k = argmax_key(Cs[r * GLDC + c] * scale, (uint32_t)(nt * 64 + c));
+      for (int c = 0; c < BN && n0 + c < V; ++c) {
+        const unsigned long long k = argmax_key(Cs[r * ldc + c] * scale, (uint32_t)(n0 + c));
         best = k > best ? k : best;
       }
       atomicMax(slot + row_stream[m0 + r], best);
@@ -125,7 +135,12 @@ struct EpiLogits {
   }
 };
 
-// ---------------------------------------------------------------- kernel
+// ---------------------------------------------------------------- generic kernel (64 x 64)
+
+// Any operand type and any K % 8 == 0 (fp32 models, odd shapes): 64x64 tile,
+// four waves of 32x32 as 16x16 MFMA fragments, K in steps of 32 through LDS.
+constexpr int GBM = 64, GBN = 64, GBK = 32;
+constexpr int GLDC = GBN + 4;
 
 template <typename TM, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm(const TM* __restrict__ A, int M, const TM* __restrict__ W, int K,
@@ -136,7 +151,7 @@ __global__ __launch_bounds__(256) void k_gemm(const TM* __restrict__ A, int M, c
   __shared__ __attribute__((aligned(16))) TM As[GBM * LDK];
   __shared__ __attribute__((aligned(16))) TM Bs[GBN * LDK];
   __shared__ float Cs[GBM * GLDC];
-  const int nt = blockIdx.x, m0 = blockIdx.y * GBM;
+  const int n0 = blockIdx.x * GBN, m0 = blockIdx.y * GBM;
   const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
   const int wm = wv >> 1, wn = wv & 1;
   const int lr = lane & 15, lk = lane >> 4;
@@ -151,7 +166,7 @@ __global__ __launch_bounds__(256) void k_gemm(const TM* __restrict__ A, int M, c
       const int r = c / CPR, kc = (c % CPR) * V;
       u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
       if (m0 + r < M && k0 + kc < K) va = *reinterpret_cast<const u32x4*>(A + (size_t)(m0 + r) * K + k0 + kc);
-      const int br = epi.b_row(nt, r);
+      const int br = epi.b_row(n0 + r);
       if (br >= 0 && k0 + kc < K) vb = *reinterpret_cast<const u32x4*>(W + (size_t)br * K + k0 + kc);
       *reinterpret_cast<u32x4*>(As + r * LDK + kc) = va;
       *reinterpret_cast<u32x4*>(Bs + r * LDK + kc) = vb;
@@ -196,38 +211,258 @@ __global__ __launch_bounds__(256) void k_gemm(const TM* __restrict__ A, int M, c
       for (int e = 0; e < 4; ++e)
         Cs[(wm * 32 + i * 16 + 4 * lk + e) * GLDC + wn * 32 + j * 16 + lr] = acc[i][j][e];
   __syncthreads();
-  epi(Cs, m0, M, nt);
+  epi(Cs, GLDC, m0, M, n0, GBM, GBN);
+}
+
+// ---------------------------------------------------------------- fp16 kernel (BM x 128 x 64)
+
+// fp16 operands, K % 64 == 0.  Tile BM x 128 (BM = 128, 64 or 32), K step 64;
+// four waves (2 x 2 for BM >= 64, else 1 x 4), each a block of 32x32x16
+// MFMAs.  Operands go global -> LDS with direct 16-byte loads arranged in MFMA
+// fragment order: one wave instruction fills one 1 KiB fragment (lane l: row
+// l%32, k 8(l/32)..+8), so every LDS read is a conflict-free 16-byte read.
+// NSTAGE stages: the loads of the next NSTAGE-1 steps are in flight while a
+// step computes; two workgroups per CU hide the rest of the latency.  Split-K
+// workgroups write fp32 partial tiles that k_splitk_finalize sums in a fixed
+// order (bitwise reproducible) before applying the epilogue.  Tiles are
+// numbered with the column index fastest, so (with workgroups dealt
+// round-robin to the 8 XCDs) row blocks that share a weight tile run on the
+// same XCD and reuse it from its L2.
+template <int BM>
+struct F16Tile {
+  static constexpr int BN = 128, BK = 64;
+  static constexpr int NSTAGE = BM == 128 ? 2 : 3;  // two workgroups per CU fit in LDS
+  static constexpr int WGM = BM >= 64 ? 2 : 1, WGN = 4 / WGM;  // wave grid
+  static constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;  // 32x32 blocks per wave
+  static constexpr int A_FR = (BM / 32) * (BK / 16);  // 1 KiB A fragments per stage
+  static constexpr int B_FR = (BN / 32) * (BK / 16);  // 1 KiB B fragments per stage
+  static constexpr int NI = (A_FR + B_FR) / 4;         // loads per wave per stage
+  static constexpr int STAGE = (A_FR + B_FR) * 1024;
+  static constexpr int LDC = BN + 4;
+  static constexpr int CS = BM * LDC * 4;
+  static constexpr int LDS = (NSTAGE * STAGE > CS ? NSTAGE * STAGE : CS);
+  static_assert((A_FR + B_FR) % 4 == 0, "fragments split evenly over four waves");
+};
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Workgroup barrier without the memory fence __syncthreads() adds (waits are
+// explicit in the caller).
+__device__ __forceinline__ void bare_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int NI>
+__device__ __forceinline__ void issue_stage(const _Float16* const* src, int koff, char* dst, int wave) {
+#pragma unroll
+  for (int q = 0; q < NI; ++q)
+    __builtin_amdgcn_global_load_lds(src[q] + koff, dst + (wave + 4 * q) * 1024, 16, 0, 0);
+}
+
+// Wait until at most n * NI of this wave's loads are outstanding (n <= 3).
+template <int NI>
+__device__ __forceinline__ void wait_stages(int n) {
+#define HH_VMWAIT(c) __builtin_amdgcn_s_waitcnt(((c) & 15) | (0x7 << 4) | (0xF << 8) | (((c) >> 4) << 14))
+  switch (n) {
+    case 0: HH_VMWAIT(0); break;
+    case 1: HH_VMWAIT(NI); break;
+    case 2: HH_VMWAIT(2 * NI); break;
+    default: HH_VMWAIT(3 * NI); break;
+  }
+#undef HH_VMWAIT
+}
+
+template <int BM, class Epi>
+__global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict__ A, int M, const _Float16* __restrict__ W,
+                                                  int K, int ntn, int ntiles, int steps_per_split,
+                                                  float* __restrict__ partial, int ncols, Epi epi) {
+  using T = F16Tile<BM>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int tile = blockIdx.x % ntiles, split = blockIdx.x / ntiles;
+  const int tn = tile % ntn, tm = tile / ntn;
+  const int m0 = tm * BM, n0 = tn * T::BN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
+  const int nk_all = K / T::BK;
+  const int s0 = split * steps_per_split;
+  const int nk = min(nk_all, s0 + steps_per_split) - s0;
+
+  // Per-lane source addresses of the fragments this wave loads (fixed over K).
+  const _Float16* src[T::NI];
+#pragma unroll
+  for (int q = 0; q < T::NI; ++q) {
+    const int f = wave + 4 * q;  // fragment index within a stage
+    if (f < T::A_FR) {
+      const int rb = f / 4, kb = f % 4;
+      const int row = min(m0 + rb * 32 + (lane & 31), M - 1);  // rows past M: computed, never stored
+      src[q] = A + (size_t)row * K + (size_t)s0 * T::BK + kb * 16 + 8 * (lane >> 5);
+    } else {
+      const int g = f - T::A_FR, cb = g / 4, kb = g % 4;
+      const int br = epi.b_row(n0 + cb * 32 + (lane & 31));
+      src[q] = W + (size_t)(br < 0 ? 0 : br) * K + (size_t)s0 * T::BK + kb * 16 + 8 * (lane >> 5);
+    }
+  }
+
+  f32x16 acc[T::FM][T::FN];
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // Waits are explicit: __syncthreads() would add a workgroup release fence,
+  // i.e. vmcnt(0), and stall on the later steps' loads as well.
+  constexpr int kWaitLds = 0xF | (0x7 << 4) | (0x3 << 14);  // lgkmcnt(0)
+  for (int i = 0; i < T::NSTAGE - 1 && i < nk; ++i)
+    issue_stage<T::NI>(src, i * T::BK, smem + i * T::STAGE, wave);
+  for (int step = 0; step < nk; ++step) {
+    const int ahead = step + T::NSTAGE - 1;
+    if (ahead < nk) issue_stage<T::NI>(src, ahead * T::BK, smem + (ahead % T::NSTAGE) * T::STAGE, wave);
+    const int later = min(T::NSTAGE - 1, nk - 1 - step);  // stages after `step` in flight
+    wait_stages<T::NI>(later);   // this wave's loads of `step` have landed
+    bare_barrier();              // ... and every other wave's
+    const char* sb = smem + (step % T::NSTAGE) * T::STAGE;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      f16x8 a[T::FM], b[T::FN];
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i)
+        a[i] = *reinterpret_cast<const f16x8*>(sb + ((wm * T::FM + i) * 4 + kb) * 1024 + lane * 16);
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+        b[j] = *reinterpret_cast<const f16x8*>(sb + (T::A_FR + (wn * T::FN + j) * 4 + kb) * 1024 + lane * 16);
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLds);  // this wave's reads of the stage are done ...
+    bare_barrier();                         // ... and every wave's, before it is refilled
+  }
+  // Result element e of lane l in a 32x32 block: row 8(e/4) + 4(l/32) + e%4, column l%32.
+  if (partial) {
+    float* dst = partial + (size_t)split * M * ncols;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = m0 + (wm * T::FM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          const int c = n0 + (wn * T::FN + j) * 32 + (lane & 31);
+          if (r < M && c < ncols) dst[(size_t)r * ncols + c] = acc[i][j][e];
+        }
+    return;
+  }
+  float* Cs = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = (wm * T::FM + i) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int c = (wn * T::FN + j) * 32 + (lane & 31);
+        Cs[r * T::LDC + c] = acc[i][j][e];
+      }
+  __syncthreads();
+  epi(Cs, T::LDC, m0, M, n0, BM, T::BN);
+}
+
+// Sum the split-K partials of a 32-row block in split order and apply the
+// epilogue (32-row blocks give the reduction enough workgroups).
+constexpr int kFinRows = 32;
+template <class Epi>
+__global__ __launch_bounds__(256) void k_splitk_finalize(const float* __restrict__ partial, int splits, int M,
+                                                         int ncols, int ntn, Epi epi) {
+  constexpr int BN = 128, LDC = BN + 4;
+  __shared__ float Cs[kFinRows * LDC];
+  const int tn = blockIdx.x % ntn, tm = blockIdx.x / ntn;
+  const int m0 = tm * kFinRows, n0 = tn * BN;
+  for (int idx = threadIdx.x; idx < kFinRows * BN; idx += 256) {
+    const int r = idx / BN, c = idx % BN;
+    float v = 0.f;
+    if (m0 + r < M && n0 + c < ncols)
+      for (int s = 0; s < splits; ++s) v += partial[((size_t)s * M + m0 + r) * ncols + n0 + c];
+    Cs[r * LDC + c] = v;
+  }
+  __syncthreads();
+  epi(Cs, LDC, m0, M, n0, kFinRows, BN);
 }
 
 // ---------------------------------------------------------------- launchers
 
-template <typename TM, typename TKV>
-void GemmKernels<TM, TKV>::qkv(hipStream_t st, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
-                               const int* row_stream, const int* row_pos, const float2* rope, float* q, TKV* kv,
-                               KvLayout L, int layer, const int* page_table) {
-  EpiQKV<TKV> e{hq, hkv, scale, row_stream, row_pos, rope, q, kv, L, layer, page_table};
-  k_gemm<TM, EpiQKV<TKV>><<<dim3(hq + 2 * hkv, (M + GBM - 1) / GBM), 256, 0, st>>>(A, M, W, d, e);
+template <int BM, class Epi>
+static void launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols, const Epi& e) {
+  using T = F16Tile<BM>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_f16<BM, Epi>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS);
+    attr = true;
+  }
+  const int ntn = (n_cols + T::BN - 1) / T::BN;
+  const int ntiles = ((M + BM - 1) / BM) * ntn;
+  const int nk = K / T::BK;
+  // Split K only when tiles alone leave most CUs idle: then aim at 256
+  // workgroups, at least 4 K steps each, with partials that fit the workspace.
+  int splits = ntiles < 128 ? (256 + ntiles - 1) / ntiles : 1;
+  splits = std::min(splits, std::max(1, nk / 4));
+  while (splits > 1 && (size_t)splits * M * n_cols * sizeof(float) > ws.bytes) --splits;
+  const int per = (nk + splits - 1) / splits;
+  splits = (nk + per - 1) / per;
+  float* part = splits > 1 ? ws.ptr : nullptr;
+  k_gemm_f16<BM, Epi><<<ntiles * splits, 256, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
+  if (splits > 1)
+    k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn, 256, 0, st>>>(part, splits, M, n_cols, ntn, e);
+}
+
+// Run C = A W^T over n_cols logical columns with epilogue e.
+template <typename TM, class Epi>
+static void run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e) {
+  if constexpr (sizeof(TM) == 2) {
+    if (K % 64 == 0) {
+      const _Float16* Ah = reinterpret_cast<const _Float16*>(A);
+      const _Float16* Wh = reinterpret_cast<const _Float16*>(W);
+      const long long ntn = (n_cols + 127) / 128;
+      if (M <= 32) launch_f16<32>(st, ws, Ah, M, Wh, K, n_cols, e);
+      else if (M <= 64 || ((M + 127) / 128) * ntn < 256) launch_f16<64>(st, ws, Ah, M, Wh, K, n_cols, e);
+      else launch_f16<128>(st, ws, Ah, M, Wh, K, n_cols, e);
+      return;
+    }
+  }
+  k_gemm<TM, Epi><<<dim3((n_cols + GBN - 1) / GBN, (M + GBM - 1) / GBM), 256, 0, st>>>(A, M, W, K, e);
 }
 
 template <typename TM, typename TKV>
-void GemmKernels<TM, TKV>::resid(hipStream_t st, const TM* A, int M, const TM* W, int K, int N, float scale,
+void GemmKernels<TM, TKV>::qkv(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
+                               const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM,
+                               TKV* kv, KvLayout L, int layer, const int* page_table) {
+  EpiQKV<TKV> e{hq, hkv, scale, row_stream, row_pos, rope, q, reinterpret_cast<TKV*>(qM), kv, L, layer, page_table};
+  run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e);
+}
+
+template <typename TM, typename TKV>
+void GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale,
                                  float* x) {
   EpiResid e{N, scale, x};
-  k_gemm<TM, EpiResid><<<dim3((N + 63) / 64, (M + GBM - 1) / GBM), 256, 0, st>>>(A, M, W, K, e);
+  run_gemm<TM>(st, ws, A, M, W, K, N, e);
 }
 
 template <typename TM, typename TKV>
-void GemmKernels<TM, TKV>::gateup(hipStream_t st, const TM* A, int M, const TM* W, int d, int F, float scale,
+void GemmKernels<TM, TKV>::gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale,
                                   TM* m) {
-  EpiGateUp<TM> e{F, scale, m};
-  k_gemm<TM, EpiGateUp<TM>><<<dim3((F + 31) / 32, (M + GBM - 1) / GBM), 256, 0, st>>>(A, M, W, d, e);
+  // Tile width: 128 on the fp16 path, 64 on the generic one; half of it gate.
+  const int bn = (sizeof(TM) == 2 && d % 64 == 0) ? 128 : GBN;
+  EpiGateUp<TM> e{F, bn / 2, scale, m};
+  run_gemm<TM>(st, ws, A, M, W, d, ((F + bn / 2 - 1) / (bn / 2)) * bn, e);
 }
 
 template <typename TM, typename TKV>
-void GemmKernels<TM, TKV>::logits(hipStream_t st, const TM* A, int M, const TM* W, int d, int V, float scale,
+void GemmKernels<TM, TKV>::logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale,
                                   float* logits, unsigned long long* slot, const int* row_stream) {
   EpiLogits e{V, scale, logits, slot, row_stream};
-  k_gemm<TM, EpiLogits><<<dim3((V + 63) / 64, (M + GBM - 1) / GBM), 256, 0, st>>>(A, M, W, d, e);
+  run_gemm<TM>(st, ws, A, M, W, d, V, e);
 }
 
 template struct GemmKernels<float, float>;

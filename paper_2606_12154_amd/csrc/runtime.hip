@@ -36,7 +36,7 @@ struct Layout {
   size_t embed, lm_head, embedM, lm_headM;
   std::vector<size_t> wqkv, wo, wgu, wdown, wqkvM, woM, wguM, wdownM, attn_norm, mlp_norm;
   size_t final_norm, rope, kv, page_table, pos, pending, slot, hist, ll, ll_words, layer_tab, trace;
-  size_t row_stream, row_pos, feed, x, h, q, o32, oM, m32, mM, part, logits, scratch_u32;
+  size_t row_stream, row_pos, feed, x, h, q, qM, o32, oM, m32, mM, part, logits, gemm_ws, gemm_ws_bytes, scratch_u32;
   size_t total;
 };
 
@@ -127,12 +127,16 @@ Layout make_layout(const hh_config& c) {
   L.x = take(R * d * 4);
   L.h = take(R * std::max(d, (size_t)hq * 64) * tm);
   L.q = take(R * hq * 64 * 4);
+  L.qM = take(R * hq * 64 * tm);
   L.o32 = take(R * hq * 64 * 4);
   L.oM = take(R * hq * 64 * tm);
   L.m32 = take(F * 4);
   L.mM = take(R * F * tm);
   L.part = take((size_t)c.max_streams * hq * kSplitMax * 66 * 4);
   L.logits = take((size_t)L.logit_rows * V * 4);
+  // Split-K partials: up to 4 splits of the widest non-head product at R rows, at most 256 MiB.
+  L.gemm_ws_bytes = std::min<size_t>((size_t)4 * R * std::max((size_t)2 * F, (size_t)L.nqkv) * 4, (size_t)256 << 20);
+  L.gemm_ws = take(L.gemm_ws_bytes);
   L.scratch_u32 = take(256);
   L.total = off;
   return L;
@@ -196,7 +200,8 @@ KvLayout kv_layout(const hh_ctx* c) { return KvLayout{c->L.n_pages, c->cfg.n_kv_
 // head_row == -1: LM head + argmax of every row (multi-stream decode);
 // head_row == -2: no head.
 template <typename TW, typename TKV, typename TM>
-void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row, float* logits) {
+void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row, float* logits,
+                    int prefill_stream = -1, int prefill_pos = 0) {
   using DK = DecodeKernels<TW, TKV, TM>;
   using GK = GemmKernels<TM, TKV>;
   const hh_config& g = c->cfg;
@@ -205,6 +210,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
   const int d = g.d_model, hq = g.n_heads, hkv = g.n_kv_heads, F = g.ffn_dim, V = g.vocab;
   const float eps = g.rms_eps, ws = 1.f / c->wscale;
   const KvLayout kl = kv_layout(c);
+  const GemmWorkspace gws{c->at<float>(L.gemm_ws), L.gemm_ws_bytes};
   int* rs = c->at<int>(L.row_stream);
   int* rp = c->at<int>(L.row_pos);
   float* x = c->at<float>(L.x);
@@ -228,12 +234,21 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       TM* oM = c->at<TM>(L.oM);
       TM* mM = c->at<TM>(L.mM);
       DK::rmsnorm_rows(st, n, x, an, eps, d, h);
-      GK::qkv(st, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, kv, kl, l, pt);
-      DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, s_max, c->at<float>(L.part), o32, oM);
-      GK::resid(st, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
+      // Prefill rows of one stream with an fp16 cache use MFMA flash attention.
+      const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv);
+      GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, flash ? c->at<TM>(L.qM) : nullptr,
+              kv, kl, l, pt);
+      if (flash) {
+        if constexpr (sizeof(TKV) == 2)
+          flash_prefill(st, reinterpret_cast<const _Float16*>(c->at<TM>(L.qM)), reinterpret_cast<const _Float16*>(kv),
+                        kl, l, pt, prefill_stream, prefill_pos, n, hq, hkv, reinterpret_cast<_Float16*>(oM));
+      } else {
+        DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, s_max, c->at<float>(L.part), o32, oM);
+      }
+      GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
       DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
-      GK::gateup(st, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM);
-      GK::resid(st, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x);
+      GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM);
+      GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x);
     }
   }
   const float* fn = c->at<float>(L.final_norm);
@@ -245,7 +260,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
     } else {
       TM* h = c->at<TM>(L.h);
       DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
-      GK::logits(st, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs);
+      GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs);
     }
   }
 }
@@ -387,7 +402,7 @@ hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, f
     HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens + r0, P * sizeof(int), hipMemcpyHostToDevice, st));
     DK::prep_embed(st, P, s, c->at<int>(L.feed), c->at<int>(L.row_stream), c->at<int>(L.row_pos), c->at<int>(L.pos),
                    c->at<int>(L.pending), c->at<TW>(L.embed), c->at<float>(L.x), c->cfg.d_model);
-    enqueue_layers<TW, TKV, TM>(c, P, false, 1, -2, nullptr);
+    enqueue_layers<TW, TKV, TM>(c, P, false, 1, -2, nullptr, s, c->len[s] + r0);
     unsigned long long* slot = c->at<unsigned long long>(L.slot);
     if (mode == HH_LOGITS_ALL) {
       for (int b0 = 0; b0 < P; b0 += kLogitRows) {
