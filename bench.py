@@ -1,17 +1,23 @@
 """Benchmark of the mouth model's hot path on one MI355X.
 
-One step = one request of the 1B-class bf16 decoder (16 layers, d 2048,
-32/8 heads, FFN 8192, vocab 128256): prefill of a 256-token uniform-random
-prompt (time to first token), then 256 greedy decode steps whose tokens are
-fed back on the device.  Weights are seeded N(0, 0.02^2) random draws rounded
-to bf16 (no trained checkpoint exists here); the prompt is uniform random ids.
+Headline workload (one "step" = one request): the 1B-class bf16 decoder (16
+layers, d 2048, 32/8 heads, FFN 8192, vocab 128256) prefills a 256-token
+uniform-random prompt (time to first token) and then runs 256 greedy decode
+steps whose tokens are fed back on the device.  Weights are seeded N(0, 0.02^2)
+draws rounded to bf16 (no trained checkpoint exists here); prompts are uniform
+random ids, which stand in exactly for the paper's rendered-answer prompts
+because a dense decoder's cost depends only on lengths.
 
-Prints ONE JSON line: decode tok/s (value), TTFT, the HBM roofline of the
-decode step, and the fp64 CPU oracle timed on a bounded sample.
+Printed: ONE JSON line with decode tok/s (value), TTFT, the HBM roofline of
+the persistent decode-step kernel (one launch per token, timed with HIP events
+on the library's stream) and the fp64 CPU oracle timed on a bounded sample.
+With --other-configs it adds context figures for the three other 1B workloads
+(1024-token prompt TTFT, 8192-token cache decode, 32 lockstep streams).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -24,19 +30,47 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "batch-1 decode tok/s + % HBM roofline; TTFT (ms) for 1B bf16 model"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_step_1b_traffic.json")
+STEP_SOURCES = ["paper_2606_12154_amd/csrc/k_step.hip", "paper_2606_12154_amd/csrc/hh_device.h",
+                "paper_2606_12154_amd/csrc/hh_kernels.h"]
 
 
-def decode_bytes_per_token(shape, t_avg: float, kv_elem: int) -> float:
-    """Algorithmic HBM bytes of one batch-1 decode token: every weight once
-    (bf16) plus the K and V of t positions in every layer."""
-    w = shape.n_params() * 2
-    kv = shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * kv_elem * t_avg
-    return w + kv
+def step_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in STEP_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def kv_bytes_per_position(shape) -> int:
+    """fp16 K and V of one position in every layer (the cache's element type)."""
+    return shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * 2
+
+
+def decode_step_bytes(shape, t: float) -> float:
+    """Algorithmic HBM bytes of one batch-1 decode launch attending t
+    positions: every bf16 weight once, the K/V of t positions, and the new
+    position's K/V write."""
+    return shape.n_params() * 2 + kv_bytes_per_position(shape) * (t + 1)
+
+
+def measured_traffic(launch_bytes: float):
+    """HBM bytes per decode-step launch from the committed counter profile,
+    or None when absent or taken on a different version of the kernel."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != step_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def cpu_baseline(shape, wseed, prompt, n_decode):
     """The fp64 oracle on the host: prefill of the prompt, then n_decode
-    cached decode steps; returns decode tok/s, prefill seconds and threads."""
+    cached decode steps; returns (decode tok/s, prefill seconds, threads)."""
     import oracle
     import synth
     try:
@@ -63,11 +97,15 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-decode-steps", type=int, default=4)
+    ap.add_argument("--other-configs", action="store_true",
+                    help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
+    ap.add_argument("--cpu-decode-steps", type=int, default=8)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: the decoder runs on a single MI355X "
-              f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
+        print(f"bench.py measures one GPU: the decoder runs on a single MI355X; "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -79,15 +117,23 @@ def main():
     shape, P, N = wl["shape"], wl["prompt"], wl["steps"]
     prompt = synth.make_tokens(shape.vocab, P, wl["tseed"])
     tensors = synth.make_weights(shape, wl["wseed"])
-    ctx = hh.Context(hh.make_config(shape, 1, P + N + 1, max_prefill=P))
+    # One context serves every 1B workload: 32 streams, 8192 + 512 positions.
+    ctx = hh.Context(hh.make_config(shape, 32, 8192 + 513, 8192))
     ctx.load_weights(tensors)
     del tensors
     st = ctx.stream
 
+    if args.calibrate_copy:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
     def one_step():
         ctx.reset(0)
         t0 = time.perf_counter()
-        nxt, _ = ctx.prefill(0, prompt)            # host ids in, host token out
+        nxt, _ = ctx.prefill(0, prompt)        # host ids in, host token out
         ttft = time.perf_counter() - t0
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -114,9 +160,11 @@ def main():
 
     dec_s = float(np.sum(decs))
     tok_s = args.steps * N / dec_s
-    t_avg = P + (N + 1) / 2.0
-    bpt = decode_bytes_per_token(shape, t_avg, 2)
-    achieved = bpt * tok_s / 1e9
+    launch_s = dec_s / (args.steps * N)          # one persistent-kernel launch per token
+    t_mean = P + (N - 1) / 2.0 + 1                # positions attended, averaged over the steps
+    launch_bytes = decode_step_bytes(shape, t_mean)
+    achieved = launch_bytes / launch_s / 1e9
+    traffic = measured_traffic(launch_bytes)
     out = {
         "metric": METRIC,
         "value": round(tok_s, 2),
@@ -130,25 +178,87 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"1B bf16 decoder, batch 1, {P}-token uniform-random prompt, "
-                               f"{N} greedy decode steps (device-fed)",
-                   "prompt": P, "decode_steps": N, "batch": 1},
+        "config": {"workload": f"1B bf16 decoder (16 layers, d 2048, 32/8 heads, FFN 8192, vocab 128256), "
+                               f"batch 1: prefill of a {P}-token uniform-random prompt, then {N} greedy "
+                               f"decode steps fed back on the device",
+                   "prompt": P, "decode_steps": N, "batch": 1, "kv_cache": "fp16, 16-token pages"},
         "ttft_ms": round(float(np.mean(ttfts)) * 1e3, 3),
         "ttft_ms_min": round(float(np.min(ttfts)) * 1e3, 3),
         "ttft_ms_max": round(float(np.max(ttfts)) * 1e3, 3),
-        "decode_ms_per_token": round(dec_s / (args.steps * N) * 1e3, 4),
-        "roofline": {"bound": "hbm", "kernel": "decode step (graph)", "achieved": round(achieved, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_token": int(bpt)},
+        "decode_ms_per_token": round(launch_s * 1e3, 4),
+        "e2e_tok_s": round(args.steps * (N + 1) / wall, 2),
+        "roofline": {"bound": "hbm", "kernel": "k_decode_step (one launch per token)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "bytes_per_launch": int(launch_bytes), "launch_us": round(launch_s * 1e6, 2)},
     }
+
+    if args.other_configs:
+        other = {}
+        # 1024-token prompt: TTFT (the prefill-dominated workload), then 64 steps.
+        w3 = synth.WORKLOADS["1b_prefill"]
+        p3 = synth.make_tokens(shape.vocab, w3["prompt"], w3["tseed"])
+        tt = []
+        for i in range(4):
+            ctx.reset(0)
+            t0 = time.perf_counter()
+            ctx.prefill(0, p3)
+            if i:
+                tt.append(time.perf_counter() - t0)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(w3["steps"]):
+            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        other["prompt1024"] = {"ttft_ms": round(float(np.mean(tt)) * 1e3, 3),
+                               "ttft_ms_min": round(float(np.min(tt)) * 1e3, 3),
+                               "prefill_tflops": round(2.062e12 / float(np.mean(tt)) / 1e12, 1),
+                               "decode_tok_s": round(w3["steps"] / (e0.elapsed_time(e1) / 1e3), 1)}
+        # 8192 positions already cached (untimed prefill), then 512 decode steps.
+        w4 = synth.WORKLOADS["1b_long"]
+        ctx.reset(0)
+        ctx.prefill(0, synth.make_tokens(shape.vocab, w4["prompt"], w4["tseed"]))
+        e0.record(st)
+        for _ in range(w4["steps"]):
+            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        s4 = e0.elapsed_time(e1) / 1e3
+        t4 = w4["prompt"] + (w4["steps"] - 1) / 2.0 + 1
+        b4 = decode_step_bytes(shape, t4)
+        other["cache8192"] = {"decode_tok_s": round(w4["steps"] / s4, 1),
+                              "hbm_frac": round(b4 * w4["steps"] / s4 / 1e9 / HBM_PEAK_GBS, 4)}
+        # 32 independent streams, 256-token prompts, lockstep decode.
+        w5 = synth.WORKLOADS["1b_multi"]
+        ctx.reset(-1)
+        ns = w5["streams"]
+        for s_ in range(ns):
+            ctx.prefill(s_, synth.make_tokens(shape.vocab, w5["prompt"], w5["tseed"] + s_))
+        hh.hh_decode_step(ctx.ctx, ns, None, None, None, None)  # first step captures the graph
+        e0.record(st)
+        n5 = w5["steps"] - 1
+        for _ in range(n5):
+            hh.hh_decode_step(ctx.ctx, ns, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        s5 = e0.elapsed_time(e1) / 1e3
+        t5 = w5["prompt"] + 1 + n5 / 2.0 + 1
+        b5 = shape.n_params() * 2 + ns * kv_bytes_per_position(shape) * (t5 + 1)
+        other["streams32"] = {"aggregate_tok_s": round(ns * n5 / s5, 1), "step_ms": round(s5 / n5 * 1e3, 3),
+                              "hbm_frac": round(b5 * n5 / s5 / 1e9 / HBM_PEAK_GBS, 4)}
+        out["other_configs"] = other
+
     ctx.close()
     del ctx
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         rate, pre_s, cores = cpu_baseline(shape, wl["wseed"], prompt, args.cpu_decode_steps)
         out["cpu_baseline"] = {"value": round(rate, 4), "unit": "tok/s", "cores": cores, "kind": "oracle",
-                               "sample": f"fp64 oracle: prefill {P} tokens ({pre_s:.2f} s, untimed for the value) "
-                                         f"then {args.cpu_decode_steps} cached decode steps"}
+                               "sample": f"fp64 numpy oracle on the same weights: prefill of the {P}-token prompt "
+                                         f"({pre_s:.1f} s, not in the rate), then {args.cpu_decode_steps} cached "
+                                         f"decode steps (rate = steps / their wall time)"}
     print(json.dumps(out), flush=True)
 
 

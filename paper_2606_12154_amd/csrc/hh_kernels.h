@@ -23,6 +23,9 @@ struct DecodeKernels {
   static void attention(hipStream_t st, int n_rows, const float* q, const TKV* kv, KvLayout L, int layer,
                         const int* page_table, const int* row_stream, const int* row_pos, int hq, int hkv, int s_max,
                         float* part, float* o32, TM* oM);
+  static void attention_rows(hipStream_t st, int n_rows, const float* q, const TKV* kv, KvLayout L, int layer,
+                             const int* page_table, const int* row_stream, const int* row_pos, int hq, int hkv,
+                             float* o32, TM* oM);
   static void rmsnorm_rows(hipStream_t st, int n_rows, const float* x, const float* gain, float eps, int d, TM* h);
 };
 

@@ -340,6 +340,98 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ p
   if (oM) oM[((size_t)r * hq + j) * 64 + lane] = (TM)out;
 }
 
+// Decode attention of row blockIdx.y for query head blockIdx.x: the 8 waves of
+// the workgroup take pages w, w + 8, ... of the row's t = pos + 1 keys (each
+// with the next page's loads in flight), keep an online softmax each, and
+// merge through LDS.  Lane (key = lane/4, quarter = lane%4) holds 16 elements
+// of one key's K and V row; reductions use DPP lane moves.
+template <typename TKV, typename TM>
+__global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, const TKV* __restrict__ kv, KvLayout L,
+                                                   int layer, const int* __restrict__ page_table,
+                                                   const int* __restrict__ row_stream, const int* __restrict__ row_pos,
+                                                   int hq, int hkv, float* __restrict__ o32, TM* __restrict__ oM) {
+  constexpr int NW = 8;
+  constexpr int KC = (int)sizeof(TKV);  // 16-byte chunks holding a lane's 16 elements
+  __shared__ float st[NW * 4 * 66];
+  const int j = blockIdx.x, r = blockIdx.y, g = j / (hq / hkv);
+  const int s = row_stream[r], t = row_pos[r] + 1, npg = (t + kPage - 1) / kPage;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, key = lane >> 2, quarter = lane & 3;
+  const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
+  float qv[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) qv[e] = q[((size_t)r * hq + j) * 64 + quarter * 16 + e] * qscale;
+  const int* pt = page_table + (size_t)s * L.max_pages;
+  u32x4 kraw[KC], vraw[KC];
+  auto load_page = [&](int pg) {
+    const int page = pt[pg];
+    const u32x4* Kp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 0, g) + key * 64 + quarter * 16);
+    const u32x4* Vp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 1, g) + key * 64 + quarter * 16);
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      kraw[c] = Kp[c];
+      vraw[c] = Vp[c];
+    }
+  };
+  float m = -INFINITY, lsum = 0.f, o[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) o[e] = 0.f;
+  if (wave < npg) load_page(wave);
+  for (int pg = wave; pg < npg; pg += NW) {
+    float kf[16], vf[16];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      widen16(kraw[c], kf + c * Vec16<TKV>::n, TKV());
+      widen16(vraw[c], vf + c * Vec16<TKV>::n, TKV());
+    }
+    if (pg + NW < npg) load_page(pg + NW);
+    float sc = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sc = fmaf(qv[e], kf[e], sc);
+    sc += dpp<0xB1>(sc);  // the 4 lanes of a key hold quarters of its dot product
+    sc += dpp<0x4E>(sc);
+    if (pg * kPage + key >= t) sc = -INFINITY;
+    const float mn = fmaxf(m, wave_max_u(sc));
+    const float alpha = exp2f(m - mn);
+    const float pk = exp2f(sc - mn);
+    lsum = lsum * alpha + (quarter == 0 ? pk : 0.f);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[e] = fmaf(pk, vf[e], o[e] * alpha);
+    m = mn;
+  }
+  lsum = wave_sum_u(lsum);
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {  // sum over the keys of each row of 16 lanes
+    float v = o[e];
+    v += dpp<0x124>(v);
+    v += dpp<0x128>(v);
+    o[e] = v;
+  }
+  float* sw = st + (wave * 4 + (lane >> 4)) * 66;
+  if ((lane & 15) == 0) {
+    sw[0] = m;
+    sw[1] = lsum;
+  }
+  if ((lane & 15) < 4) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sw[2 + quarter * 16 + e] = o[e];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float M = -INFINITY;
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, st[w * 4 * 66]);
+    float Ls = 0.f, O = 0.f;
+    for (int w = 0; w < NW; ++w) {
+      const float* sv = st + w * 4 * 66;
+      const float f = exp2f(sv[0] - M);  // 0 for waves without pages
+      Ls = fmaf(sv[1], f, Ls);
+      O = fmaf((sv[2 + lane] + sv[66 + 2 + lane]) + (sv[132 + 2 + lane] + sv[198 + 2 + lane]), f, O);
+    }
+    const float out = O / Ls;
+    o32[((size_t)r * hq + j) * 64 + lane] = out;
+    if (oM) oM[((size_t)r * hq + j) * 64 + lane] = (TM)out;
+  }
+}
+
 // ---------------------------------------------------------------- rows RMSNorm
 
 // h[r] = x[r] * rsqrt(mean(x[r]^2) + eps) * gain, stored as the MFMA operand type.
@@ -402,6 +494,14 @@ void DecodeKernels<TW, TKV, TM>::attention(hipStream_t st, int n_rows, const flo
                                         oM);
   if (s_max > 1)
     k_attn_combine<TM><<<dim3(hq, n_rows), 64, 0, st>>>(part, row_pos, hq, s_max, o32, oM);
+}
+
+template <typename TW, typename TKV, typename TM>
+void DecodeKernels<TW, TKV, TM>::attention_rows(hipStream_t st, int n_rows, const float* q, const TKV* kv,
+                                                KvLayout L, int layer, const int* page_table, const int* row_stream,
+                                                const int* row_pos, int hq, int hkv, float* o32, TM* oM) {
+  k_attn_rows<TKV, TM><<<dim3(hq, n_rows), 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, hkv,
+                                                         o32, oM);
 }
 
 template <typename TW, typename TKV, typename TM>

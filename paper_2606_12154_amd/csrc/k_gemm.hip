@@ -369,9 +369,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict_
   epi(Cs, T::LDC, m0, M, n0, BM, T::BN);
 }
 
-// Sum the split-K partials of a 32-row block in split order and apply the
-// epilogue (32-row blocks give the reduction enough workgroups).
-constexpr int kFinRows = 32;
+// Sum the split-K partials of a 2-row block in split order and apply the
+// epilogue (small blocks give the reduction enough workgroups; each thread
+// sums one element's partials with independent loads).
+constexpr int kFinRows = 2;
 template <class Epi>
 __global__ __launch_bounds__(256) void k_splitk_finalize(const float* __restrict__ partial, int splits, int M,
                                                          int ncols, int ntn, Epi epi) {
@@ -382,8 +383,19 @@ __global__ __launch_bounds__(256) void k_splitk_finalize(const float* __restrict
   for (int idx = threadIdx.x; idx < kFinRows * BN; idx += 256) {
     const int r = idx / BN, c = idx % BN;
     float v = 0.f;
-    if (m0 + r < M && n0 + c < ncols)
-      for (int s = 0; s < splits; ++s) v += partial[((size_t)s * M + m0 + r) * ncols + n0 + c];
+    if (m0 + r < M && n0 + c < ncols) {
+      const float* pp = partial + (size_t)(m0 + r) * ncols + n0 + c;
+      const size_t stride = (size_t)M * ncols;
+      int sp = 0;
+      for (; sp + 4 <= splits; sp += 4) {
+        const float a = pp[sp * stride], b = pp[(sp + 1) * stride], c2 = pp[(sp + 2) * stride], d = pp[(sp + 3) * stride];
+        v += a;  // split order, as in the loop below
+        v += b;
+        v += c2;
+        v += d;
+      }
+      for (; sp < splits; ++sp) v += pp[sp * stride];
+    }
     Cs[r * LDC + c] = v;
   }
   __syncthreads();

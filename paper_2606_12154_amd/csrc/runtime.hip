@@ -225,7 +225,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
     const float* mn = c->at<float>(L.mlp_norm[l]);
     if (decode_gemv) {
       DK::qkv_gemv(st, c->at<TW>(L.wqkv[l]), x, an, eps, d, hq, hkv, rs, rp, rope, q, kv, kl, l, pt);
-      DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, s_max, c->at<float>(L.part), o32, nullptr);
+      DK::attention_rows(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, o32, nullptr);
       DK::resid_gemv(st, c->at<TW>(L.wo[l]), o32, hq * 64, d, x);
       DK::gateup_gemv(st, c->at<TW>(L.wgu[l]), x, mn, eps, d, F, c->at<float>(L.m32));
       DK::resid_gemv(st, c->at<TW>(L.wdown[l]), c->at<float>(L.m32), F, d, x);
@@ -242,8 +242,10 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
         if constexpr (sizeof(TKV) == 2)
           flash_prefill(st, reinterpret_cast<const _Float16*>(c->at<TM>(L.qM)), reinterpret_cast<const _Float16*>(kv),
                         kl, l, pt, prefill_stream, prefill_pos, n, hq, hkv, reinterpret_cast<_Float16*>(oM));
+      } else if (prefill_stream >= 0) {
+        DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, 1, c->at<float>(L.part), o32, oM);
       } else {
-        DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, s_max, c->at<float>(L.part), o32, oM);
+        DK::attention_rows(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, o32, oM);
       }
       GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
       DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
