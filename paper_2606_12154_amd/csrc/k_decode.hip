@@ -208,6 +208,105 @@ __global__ __launch_bounds__(256) void k_gateup_gemv(const TW* __restrict__ W, c
     m[blockIdx.x * 4 + threadIdx.x] = silu(res[threadIdx.x]) * res[4 + threadIdx.x];
 }
 
+// Final RMSNorm + LM head for one row `row` of x, streaming: two blocks per
+// CU each stage the normalised vector once and take an equal share of the
+// rows, each wave one row at a time (lane l: 16-byte chunks l, l + 64,
+// l + 128, l + 192) with its next two rows' loads in flight in two more
+// register sets (strict rotation: no register copy, so the compiler waits for
+// exactly the oldest set).  Writes optional fp32 logits and a packed
+// (value, index) atomicMax into the stream's argmax slot.  Rows need at most
+// 4 chunks per lane (d * sizeof(TW) <= 4096).
+template <typename TW>
+__device__ __forceinline__ void head_row_loads(u32x4* w, const TW* __restrict__ W, int row, int nch) {
+  const u32x4* src = reinterpret_cast<const u32x4*>(W + (size_t)row * nch * Vec16<TW>::n);
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) w[c] = __builtin_nontemporal_load(src + min(lane + 64 * c, nch - 1));
+}
+
+template <typename TW>
+__device__ __forceinline__ float head_row_dot(const u32x4* w, const float* xs, int nch) {
+  constexpr int V = Vec16<TW>::n;
+  const int lane = threadIdx.x & 63;
+  float acc = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = lane + 64 * c;
+    const bool in = ch < nch;
+    const float4* xc = reinterpret_cast<const float4*>(xs + (in ? ch : nch - 1) * V);
+    float wf[V], xv[V];
+    widen16(w[c], wf, TW());
+#pragma unroll
+    for (int e = 0; e < V / 4; ++e) {  // 16-byte LDS reads; the select acts on the values
+      const float4 t = xc[e];
+      xv[4 * e] = in ? t.x : 0.f;
+      xv[4 * e + 1] = in ? t.y : 0.f;
+      xv[4 * e + 2] = in ? t.z : 0.f;
+      xv[4 * e + 3] = in ? t.w : 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc = fmaf(wf[e], xv[e], acc);
+  }
+  return wave_sum(acc);
+}
+
+template <typename TW>
+__global__ __launch_bounds__(256) void k_head_stream(const TW* __restrict__ W, const float* __restrict__ x,
+                                                     const float* __restrict__ gain, float eps, int d, int V, int row,
+                                                     const int* __restrict__ row_stream, float* __restrict__ logits,
+                                                     unsigned long long* __restrict__ slot) {
+  extern __shared__ float xs[];
+  __shared__ float red[4];
+  __shared__ unsigned long long kred[4];
+  stage_vector(x + (size_t)row * d, gain, eps, d, xs, red);
+  const int r0 = (int)(((long long)V * blockIdx.x) / gridDim.x), r1 = (int)(((long long)V * (blockIdx.x + 1)) / gridDim.x);
+  if (r0 >= r1) return;
+  const int nch = d / Vec16<TW>::n;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned long long best = 0ull;
+  auto take = [&](const u32x4* w, int r) {
+    const float v = head_row_dot<TW>(w, xs, nch);
+    if (lane == 0) {
+      if (logits) logits[r] = v;
+      const unsigned long long k = argmax_key(v, (uint32_t)r);
+      best = k > best ? k : best;
+    }
+  };
+  // Rows r0 + wave, + 4, ...; loads past r1 re-read the block's last row.
+  u32x4 a[4], b[4], c[4];
+  head_row_loads<TW>(a, W, min(r0 + wave, r1 - 1), nch);
+  head_row_loads<TW>(b, W, min(r0 + wave + 4, r1 - 1), nch);
+  for (int r = r0 + wave; r < r1; r += 12) {
+    head_row_loads<TW>(c, W, min(r + 8, r1 - 1), nch);
+    take(a, r);
+    if (r + 4 >= r1) break;
+    head_row_loads<TW>(a, W, min(r + 12, r1 - 1), nch);
+    take(b, r + 4);
+    if (r + 8 >= r1) break;
+    head_row_loads<TW>(b, W, min(r + 16, r1 - 1), nch);
+    take(c, r + 8);
+  }
+  if (lane == 0) kred[wave] = best;
+  __syncthreads();
+  if (threadIdx.x == 0 && slot) {
+    for (int w = 1; w < 4; ++w) best = kred[w] > best ? kred[w] : best;
+    atomicMax(slot + row_stream[row], best);
+  }
+}
+
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 // Final RMSNorm + LM head rows [8b, 8b + 8) < V for decode row `row`:
 // optional fp32 logits, and a packed (value, index) atomicMax into the
 // stream's argmax slot (slot == nullptr: logits only).
@@ -481,7 +580,12 @@ template <typename TW, typename TKV, typename TM>
 void DecodeKernels<TW, TKV, TM>::head_gemv(hipStream_t st, const TW* W, const float* x, const float* gain, float eps,
                                            int d, int V, int row, const int* row_stream, float* logits,
                                            unsigned long long* slot) {
-  k_head_gemv<TW><<<(V + 7) / 8, 256, d * sizeof(float), st>>>(W, x, gain, eps, d, V, row, row_stream, logits, slot);
+  if (d / Vec16<TW>::n <= 256)
+    k_head_stream<TW><<<2 * device_cus(), 256, d * sizeof(float), st>>>(W, x, gain, eps, d, V, row, row_stream,
+                                                                        logits, slot);
+  else
+    k_head_gemv<TW><<<(V + 7) / 8, 256, d * sizeof(float), st>>>(W, x, gain, eps, d, V, row, row_stream, logits,
+                                                                  slot);
 }
 
 template <typename TW, typename TKV, typename TM>

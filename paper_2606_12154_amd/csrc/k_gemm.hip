@@ -218,9 +218,10 @@ __global__ __launch_bounds__(256) void k_gemm(const TM* __restrict__ A, int M, c
 
 // fp16 operands, K % 64 == 0.  Tile BM x 128 (BM = 128, 64 or 32), K step 64;
 // four waves (2 x 2 for BM >= 64, else 1 x 4), each a block of 32x32x16
-// MFMAs.  Operands go global -> LDS with direct 16-byte loads arranged in MFMA
-// fragment order: one wave instruction fills one 1 KiB fragment (lane l: row
-// l%32, k 8(l/32)..+8), so every LDS read is a conflict-free 16-byte read.
+// MFMAs.  Operands go global -> LDS with direct 16-byte loads, a wave
+// instruction moving 8 whole rows of the step (8 cache lines) into an
+// XOR-swizzled row-major stage, so every MFMA fragment read is a
+// conflict-free 16-byte read.
 // NSTAGE stages: the loads of the next NSTAGE-1 steps are in flight while a
 // step computes; two workgroups per CU hide the rest of the latency.  Split-K
 // workgroups write fp32 partial tiles that k_splitk_finalize sums in a fixed
@@ -234,14 +235,13 @@ struct F16Tile {
   static constexpr int NSTAGE = BM == 128 ? 2 : 3;  // two workgroups per CU fit in LDS
   static constexpr int WGM = BM >= 64 ? 2 : 1, WGN = 4 / WGM;  // wave grid
   static constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;  // 32x32 blocks per wave
-  static constexpr int A_FR = (BM / 32) * (BK / 16);  // 1 KiB A fragments per stage
-  static constexpr int B_FR = (BN / 32) * (BK / 16);  // 1 KiB B fragments per stage
-  static constexpr int NI = (A_FR + B_FR) / 4;         // loads per wave per stage
-  static constexpr int STAGE = (A_FR + B_FR) * 1024;
+  static constexpr int GROUPS = (BM + BN) / 8;        // 1 KiB row groups (8 rows x 64 k) per stage
+  static constexpr int NI = GROUPS / 4;                // loads per wave per stage
+  static constexpr int STAGE = GROUPS * 1024;
   static constexpr int LDC = BN + 4;
   static constexpr int CS = BM * LDC * 4;
   static constexpr int LDS = (NSTAGE * STAGE > CS ? NSTAGE * STAGE : CS);
-  static_assert((A_FR + B_FR) % 4 == 0, "fragments split evenly over four waves");
+  static_assert(GROUPS % 4 == 0, "row groups split evenly over four waves");
 };
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -271,10 +271,12 @@ __device__ __forceinline__ void wait_stages(int n) {
 }
 
 template <int BM, class Epi>
-__global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict__ A, int M, const _Float16* __restrict__ W,
-                                                  int K, int ntn, int ntiles, int steps_per_split,
-                                                  float* __restrict__ partial, int ncols, Epi epi) {
+__global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict__ A, int M,
+                                                  const _Float16* __restrict__ W, int K, int ntn, int ntiles,
+                                                  int steps_per_split, float* __restrict__ partial, int ncols,
+                                                  Epi epi) {
   using T = F16Tile<BM>;
+  static_assert((T::NSTAGE - 1) * T::NI <= 63, "in-flight loads exceed the vmcnt range");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tile = blockIdx.x % ntiles, split = blockIdx.x / ntiles;
   const int tn = tile % ntn, tm = tile / ntn;
@@ -285,19 +287,24 @@ __global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict_
   const int s0 = split * steps_per_split;
   const int nk = min(nk_all, s0 + steps_per_split) - s0;
 
-  // Per-lane source addresses of the fragments this wave loads (fixed over K).
+  // Per-lane source addresses of the row groups this wave loads (fixed over
+  // K).  A stage holds the BM rows of A then the BN rows of W, 128 bytes (the
+  // step's 64 k) each; instruction q of wave w fills row group g = w + 4q
+  // (rows 8g .. 8g + 7, 1 KiB): lane l takes row 8g + l/8 and stores it in
+  // slot l%8, which holds the row's k chunk (l%8) ^ (row%8).  Each
+  // instruction thus reads 8 whole cache lines, and the swizzle keeps the
+  // MFMA fragment reads (8 consecutive rows, one chunk) conflict-free.
   const _Float16* src[T::NI];
 #pragma unroll
   for (int q = 0; q < T::NI; ++q) {
-    const int f = wave + 4 * q;  // fragment index within a stage
-    if (f < T::A_FR) {
-      const int rb = f / 4, kb = f % 4;
-      const int row = min(m0 + rb * 32 + (lane & 31), M - 1);  // rows past M: computed, never stored
-      src[q] = A + (size_t)row * K + (size_t)s0 * T::BK + kb * 16 + 8 * (lane >> 5);
+    const int rr = 8 * (wave + 4 * q) + (lane >> 3);  // row within the stage
+    const int chunk = (lane & 7) ^ (lane >> 3);
+    if (rr < BM) {
+      const int row = min(m0 + rr, M - 1);  // rows past M: computed, never stored
+      src[q] = A + (size_t)row * K + (size_t)s0 * T::BK + chunk * 8;
     } else {
-      const int g = f - T::A_FR, cb = g / 4, kb = g % 4;
-      const int br = epi.b_row(n0 + cb * 32 + (lane & 31));
-      src[q] = W + (size_t)(br < 0 ? 0 : br) * K + (size_t)s0 * T::BK + kb * 16 + 8 * (lane >> 5);
+      const int br = epi.b_row(n0 + rr - BM);
+      src[q] = W + (size_t)(br < 0 ? 0 : br) * K + (size_t)s0 * T::BK + chunk * 8;
     }
   }
 
@@ -321,15 +328,19 @@ __global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict_
     wait_stages<T::NI>(later);   // this wave's loads of `step` have landed
     bare_barrier();              // ... and every other wave's
     const char* sb = smem + (step % T::NSTAGE) * T::STAGE;
+    // Fragment of rows r0 .. r0 + 31, k 16 kb .. + 16: lane l reads row
+    // r0 + l%32, chunk 2 kb + l/32, from its swizzled slot.
+    auto frag = [&](int r0, int kb) {
+      const int r = r0 + (lane & 31), c = 2 * kb + (lane >> 5);
+      return *reinterpret_cast<const f16x8*>(sb + r * 128 + 16 * (c ^ (r & 7)));
+    };
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       f16x8 a[T::FM], b[T::FN];
 #pragma unroll
-      for (int i = 0; i < T::FM; ++i)
-        a[i] = *reinterpret_cast<const f16x8*>(sb + ((wm * T::FM + i) * 4 + kb) * 1024 + lane * 16);
+      for (int i = 0; i < T::FM; ++i) a[i] = frag((wm * T::FM + i) * 32, kb);
 #pragma unroll
-      for (int j = 0; j < T::FN; ++j)
-        b[j] = *reinterpret_cast<const f16x8*>(sb + (T::A_FR + (wn * T::FN + j) * 4 + kb) * 1024 + lane * 16);
+      for (int j = 0; j < T::FN; ++j) b[j] = frag(BM + (wn * T::FN + j) * 32, kb);
 #pragma unroll
       for (int i = 0; i < T::FM; ++i)
 #pragma unroll

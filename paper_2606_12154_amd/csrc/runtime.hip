@@ -235,7 +235,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       TM* mM = c->at<TM>(L.mM);
       DK::rmsnorm_rows(st, n, x, an, eps, d, h);
       // Prefill rows of one stream with an fp16 cache use MFMA flash attention.
-      const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv);
+      const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv, c->cfg.max_context);
       GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, flash ? c->at<TM>(L.qM) : nullptr,
               kv, kl, l, pt);
       if (flash) {
