@@ -232,16 +232,22 @@ __global__ __launch_bounds__(256) void k_gemm(const TM* __restrict__ A, int M, c
 template <int BM>
 struct F16Tile {
   static constexpr int BN = 128, BK = 64;
-  static constexpr int NSTAGE = BM == 128 ? 2 : 3;  // two workgroups per CU fit in LDS
-  static constexpr int WGM = BM >= 64 ? 2 : 1, WGN = 4 / WGM;  // wave grid
+  // Four waves; two workgroups per CU fit in LDS (two independent
+  // workgroups hide each other's barrier and load stalls better than one
+  // workgroup of eight waves with a deeper pipeline).
+  static constexpr int NW = 4;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int OCC = 2;
+  static constexpr int NSTAGE = BM == 128 ? 2 : 3;
+  static constexpr int WGM = BM >= 64 ? 2 : 1, WGN = NW / WGM;  // wave grid
   static constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;  // 32x32 blocks per wave
   static constexpr int GROUPS = (BM + BN) / 8;        // 1 KiB row groups (8 rows x 64 k) per stage
-  static constexpr int NI = GROUPS / 4;                // loads per wave per stage
+  static constexpr int NI = GROUPS / NW;               // loads per wave per stage
   static constexpr int STAGE = GROUPS * 1024;
   static constexpr int LDC = BN + 4;
   static constexpr int CS = BM * LDC * 4;
   static constexpr int LDS = (NSTAGE * STAGE > CS ? NSTAGE * STAGE : CS);
-  static_assert(GROUPS % 4 == 0, "row groups split evenly over four waves");
+  static_assert(GROUPS % NW == 0, "row groups split evenly over the waves");
 };
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -250,11 +256,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // explicit in the caller).
 __device__ __forceinline__ void bare_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int NI>
+template <int NI, int NW>
 __device__ __forceinline__ void issue_stage(const _Float16* const* src, int koff, char* dst, int wave) {
 #pragma unroll
   for (int q = 0; q < NI; ++q)
-    __builtin_amdgcn_global_load_lds(src[q] + koff, dst + (wave + 4 * q) * 1024, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(src[q] + koff, dst + (wave + NW * q) * 1024, 16, 0, 0);
 }
 
 // Wait until at most n * NI of this wave's loads are outstanding (n <= 3).
@@ -271,7 +277,7 @@ __device__ __forceinline__ void wait_stages(int n) {
 }
 
 template <int BM, class Epi>
-__global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict__ A, int M,
+__global__ __launch_bounds__(F16Tile<BM>::THREADS, F16Tile<BM>::OCC) void k_gemm_f16(const _Float16* __restrict__ A, int M,
                                                   const _Float16* __restrict__ W, int K, int ntn, int ntiles,
                                                   int steps_per_split, float* __restrict__ partial, int ncols,
                                                   Epi epi) {
@@ -290,15 +296,16 @@ __global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict_
   // Per-lane source addresses of the row groups this wave loads (fixed over
   // K).  A stage holds the BM rows of A then the BN rows of W, 128 bytes (the
   // step's 64 k) each; instruction q of wave w fills row group g = w + 4q
-  // (rows 8g .. 8g + 7, 1 KiB): lane l takes row 8g + l/8 and stores it in
-  // slot l%8, which holds the row's k chunk (l%8) ^ (row%8).  Each
-  // instruction thus reads 8 whole cache lines, and the swizzle keeps the
-  // MFMA fragment reads (8 consecutive rows, one chunk) conflict-free.
+  // (rows 8g .. 8g + 7, 1 KiB; g = w + NW q): lane l takes row r = 8g + l/8 and stores it
+  // in slot l%8, which holds the row's k chunk (l%8) ^ swz(r), swz(r) =
+  // (r/2)%8.  Each instruction thus reads 8 whole cache lines, and an MFMA
+  // fragment read (16 consecutive rows, one chunk, per 64-bank cycle) hits
+  // 16 distinct bank quads.
   const _Float16* src[T::NI];
 #pragma unroll
   for (int q = 0; q < T::NI; ++q) {
-    const int rr = 8 * (wave + 4 * q) + (lane >> 3);  // row within the stage
-    const int chunk = (lane & 7) ^ (lane >> 3);
+    const int rr = 8 * (wave + T::NW * q) + (lane >> 3);  // row within the stage
+    const int chunk = (lane & 7) ^ ((rr >> 1) & 7);
     if (rr < BM) {
       const int row = min(m0 + rr, M - 1);  // rows past M: computed, never stored
       src[q] = A + (size_t)row * K + (size_t)s0 * T::BK + chunk * 8;
@@ -320,10 +327,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict_
   // i.e. vmcnt(0), and stall on the later steps' loads as well.
   constexpr int kWaitLds = 0xF | (0x7 << 4) | (0x3 << 14);  // lgkmcnt(0)
   for (int i = 0; i < T::NSTAGE - 1 && i < nk; ++i)
-    issue_stage<T::NI>(src, i * T::BK, smem + i * T::STAGE, wave);
+    issue_stage<T::NI, T::NW>(src, i * T::BK, smem + i * T::STAGE, wave);
   for (int step = 0; step < nk; ++step) {
     const int ahead = step + T::NSTAGE - 1;
-    if (ahead < nk) issue_stage<T::NI>(src, ahead * T::BK, smem + (ahead % T::NSTAGE) * T::STAGE, wave);
+    if (ahead < nk) issue_stage<T::NI, T::NW>(src, ahead * T::BK, smem + (ahead % T::NSTAGE) * T::STAGE, wave);
     const int later = min(T::NSTAGE - 1, nk - 1 - step);  // stages after `step` in flight
     wait_stages<T::NI>(later);   // this wave's loads of `step` have landed
     bare_barrier();              // ... and every other wave's
@@ -332,7 +339,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_f16(const _Float16* __restrict_
     // r0 + l%32, chunk 2 kb + l/32, from its swizzled slot.
     auto frag = [&](int r0, int kb) {
       const int r = r0 + (lane & 31), c = 2 * kb + (lane >> 5);
-      return *reinterpret_cast<const f16x8*>(sb + r * 128 + 16 * (c ^ (r & 7)));
+      return *reinterpret_cast<const f16x8*>(sb + r * 128 + 16 * (c ^ ((r >> 1) & 7)));
     };
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
@@ -435,7 +442,7 @@ static void launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
   const int per = (nk + splits - 1) / splits;
   splits = (nk + per - 1) / per;
   float* part = splits > 1 ? ws.ptr : nullptr;
-  k_gemm_f16<BM, Epi><<<ntiles * splits, 256, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
+  k_gemm_f16<BM, Epi><<<ntiles * splits, T::THREADS, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
   if (splits > 1)
     k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn, 256, 0, st>>>(part, splits, M, n_cols, ntn, e);
 }
