@@ -439,91 +439,142 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ p
   if (oM) oM[((size_t)r * hq + j) * 64 + lane] = (TM)out;
 }
 
-// Decode attention of row blockIdx.y for query head blockIdx.x: the 8 waves of
-// the workgroup take pages w, w + 8, ... of the row's t = pos + 1 keys (each
-// with the next page's loads in flight), keep an online softmax each, and
-// merge through LDS.  Lane (key = lane/4, quarter = lane%4) holds 16 elements
-// of one key's K and V row; reductions use DPP lane moves.
-template <typename TKV, typename TM>
+// Paged GQA attention for decode rows: one 512-thread workgroup per (row,
+// kv head) serves the G query heads of that kv head, so each K/V page is
+// read once.  The row's page list is staged in LDS; wave w takes pages w,
+// w + 8, ... with the next page's K/V in flight in a second register set
+// (strict alternation, no register copies).  Lane (key = lane / 4, quarter =
+// lane % 4) holds 16 dims of one key; scores use exp2 with 1/sqrt(64)*log2(e)
+// folded into q; each head keeps its own online softmax state.  The waves'
+// states are merged in LDS, one wave per head.
+constexpr int kRowsMaxPages = 2048;  // pages of one row (32768 positions)
+
+template <typename TKV>
+struct KvPage {
+  u32x4 k[sizeof(TKV)], v[sizeof(TKV)];  // 16 elements of a key: 2 chunks (fp16) or 4 (fp32)
+};
+
+template <typename TKV>
+__device__ __forceinline__ void kv_page_load(KvPage<TKV>& P, const TKV* __restrict__ kv, const KvLayout& L, int layer,
+                                             int page, int g, int key, int quarter) {
+  const u32x4* Kp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 0, g) + key * 64 + quarter * 16);
+  const u32x4* Vp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 1, g) + key * 64 + quarter * 16);
+#pragma unroll
+  for (int c = 0; c < (int)sizeof(TKV); ++c) {
+    P.k[c] = Kp[c];
+    P.v[c] = Vp[c];
+  }
+}
+
+template <typename TKV, typename TM, int G>
 __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, const TKV* __restrict__ kv, KvLayout L,
                                                    int layer, const int* __restrict__ page_table,
                                                    const int* __restrict__ row_stream, const int* __restrict__ row_pos,
-                                                   int hq, int hkv, float* __restrict__ o32, TM* __restrict__ oM) {
+                                                   int hq, float* __restrict__ o32, TM* __restrict__ oM) {
   constexpr int NW = 8;
-  constexpr int KC = (int)sizeof(TKV);  // 16-byte chunks holding a lane's 16 elements
-  __shared__ float st[NW * 4 * 66];
-  const int j = blockIdx.x, r = blockIdx.y, g = j / (hq / hkv);
+  constexpr int SLOT = 66;  // m, l, o[64]
+  __shared__ float st[NW * G * 4 * SLOT];
+  __shared__ int pts[kRowsMaxPages];
+  const int g = blockIdx.x, r = blockIdx.y;
   const int s = row_stream[r], t = row_pos[r] + 1, npg = (t + kPage - 1) / kPage;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, key = lane >> 2, quarter = lane & 3;
   const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
-  float qv[16];
+  for (int i = threadIdx.x; i < npg; i += 512) pts[i] = page_table[(size_t)s * L.max_pages + i];
+  float qv[G][16];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) qv[e] = q[((size_t)r * hq + j) * 64 + quarter * 16 + e] * qscale;
-  const int* pt = page_table + (size_t)s * L.max_pages;
-  u32x4 kraw[KC], vraw[KC];
-  auto load_page = [&](int pg) {
-    const int page = pt[pg];
-    const u32x4* Kp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 0, g) + key * 64 + quarter * 16);
-    const u32x4* Vp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 1, g) + key * 64 + quarter * 16);
+  for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      kraw[c] = Kp[c];
-      vraw[c] = Vp[c];
-    }
-  };
-  float m = -INFINITY, lsum = 0.f, o[16];
+    for (int e = 0; e < 16; ++e) qv[h][e] = q[((size_t)r * hq + g * G + h) * 64 + quarter * 16 + e] * qscale;
+  __syncthreads();
+
+  float m[G], lsum[G], o[G][16];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) o[e] = 0.f;
-  if (wave < npg) load_page(wave);
-  for (int pg = wave; pg < npg; pg += NW) {
+  for (int h = 0; h < G; ++h) {
+    m[h] = -INFINITY;
+    lsum[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[h][e] = 0.f;
+  }
+  auto take = [&](const KvPage<TKV>& P, int pg) {
     float kf[16], vf[16];
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      widen16(kraw[c], kf + c * Vec16<TKV>::n, TKV());
-      widen16(vraw[c], vf + c * Vec16<TKV>::n, TKV());
+    for (int c = 0; c < (int)sizeof(TKV); ++c) {
+      widen16(P.k[c], kf + c * Vec16<TKV>::n, TKV());
+      widen16(P.v[c], vf + c * Vec16<TKV>::n, TKV());
     }
-    if (pg + NW < npg) load_page(pg + NW);
-    float sc = 0.f;
+    const bool valid = pg * kPage + key < t;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) sc = fmaf(qv[e], kf[e], sc);
-    sc += dpp<0xB1>(sc);  // the 4 lanes of a key hold quarters of its dot product
-    sc += dpp<0x4E>(sc);
-    if (pg * kPage + key >= t) sc = -INFINITY;
-    const float mn = fmaxf(m, wave_max_u(sc));
-    const float alpha = exp2f(m - mn);
-    const float pk = exp2f(sc - mn);
-    lsum = lsum * alpha + (quarter == 0 ? pk : 0.f);
+    for (int h = 0; h < G; ++h) {
+      float a0 = 0.f, a1 = 0.f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) o[e] = fmaf(pk, vf[e], o[e] * alpha);
-    m = mn;
+      for (int e = 0; e < 16; e += 2) {
+        a0 = fmaf(qv[h][e], kf[e], a0);
+        a1 = fmaf(qv[h][e + 1], kf[e + 1], a1);
+      }
+      float sc = a0 + a1;
+      sc += dpp<0xB1>(sc);  // the 4 lanes of a key hold quarters of its dot product
+      sc += dpp<0x4E>(sc);
+      if (!valid) sc = -INFINITY;
+      const float mn = fmaxf(m[h], wave_max_u(sc));  // finite: every page has a valid key
+      const float alpha = exp2f(m[h] - mn);
+      const float pk = exp2f(sc - mn);
+      lsum[h] = lsum[h] * alpha + (quarter == 0 ? pk : 0.f);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[h][e] = fmaf(pk, vf[e], o[h][e] * alpha);
+      m[h] = mn;
+    }
+  };
+  // Pages wave, wave + 8, ...; loads past the end re-read the row's last page.
+  if (wave < npg) {
+    KvPage<TKV> A, B;
+    kv_page_load(A, kv, L, layer, pts[wave], g, key, quarter);
+    for (int pg = wave; pg < npg; pg += 2 * NW) {
+      kv_page_load(B, kv, L, layer, pts[min(pg + NW, npg - 1)], g, key, quarter);
+      take(A, pg);
+      if (pg + NW >= npg) break;
+      kv_page_load(A, kv, L, layer, pts[min(pg + 2 * NW, npg - 1)], g, key, quarter);
+      take(B, pg + NW);
+    }
   }
-  lsum = wave_sum_u(lsum);
+  // Per head: reduce over the keys of each row of 16 lanes (lanes sharing
+  // `quarter`; row_ror by 4 and 8 keeps lane bits 0-1), leave row partials in
+  // the wave's slots; waves without pages leave m = -inf, l = 0, o = 0.
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {  // sum over the keys of each row of 16 lanes
-    float v = o[e];
-    v += dpp<0x124>(v);
-    v += dpp<0x128>(v);
-    o[e] = v;
-  }
-  float* sw = st + (wave * 4 + (lane >> 4)) * 66;
-  if ((lane & 15) == 0) {
-    sw[0] = m;
-    sw[1] = lsum;
-  }
-  if ((lane & 15) < 4) {
+  for (int h = 0; h < G; ++h) {
+    const float ls = wave_sum_u(lsum[h]);
+    float* sw = st + ((wave * G + h) * 4 + (lane >> 4)) * SLOT;
+    if ((lane & 15) == 0) {
+      sw[0] = m[h];
+      sw[1] = ls;
+    }
 #pragma unroll
-    for (int e = 0; e < 16; ++e) sw[2 + quarter * 16 + e] = o[e];
+    for (int e = 0; e < 16; ++e) {
+      float v = o[h][e];
+      v += dpp<0x124>(v);
+      v += dpp<0x128>(v);
+      if ((lane & 15) < 4) sw[2 + quarter * 16 + e] = v;
+    }
   }
   __syncthreads();
-  if (wave == 0) {
-    float M = -INFINITY;
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, st[w * 4 * 66]);
-    float Ls = 0.f, O = 0.f;
+  if (wave < G) {
+    const int h = wave, j = g * G + h;
+    float Mg[NW], Lg[NW], Og[NW];
+#pragma unroll
     for (int w = 0; w < NW; ++w) {
-      const float* sv = st + w * 4 * 66;
-      const float f = exp2f(sv[0] - M);  // 0 for waves without pages
-      Ls = fmaf(sv[1], f, Ls);
-      O = fmaf((sv[2 + lane] + sv[66 + 2 + lane]) + (sv[132 + 2 + lane] + sv[198 + 2 + lane]), f, O);
+      const float* sv = st + (w * G + h) * 4 * SLOT;
+      Mg[w] = sv[0];
+      Lg[w] = sv[1];
+      Og[w] = (sv[2 + lane] + sv[SLOT + 2 + lane]) + (sv[2 * SLOT + 2 + lane] + sv[3 * SLOT + 2 + lane]);
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, Mg[w]);
+    float Ls = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = Mg[w] > -INFINITY ? exp2f(Mg[w] - M) : 0.f;
+      Ls = fmaf(Lg[w], f, Ls);
+      O = fmaf(Og[w], f, O);
     }
     const float out = O / Ls;
     o32[((size_t)r * hq + j) * 64 + lane] = out;
@@ -604,8 +655,13 @@ template <typename TW, typename TKV, typename TM>
 void DecodeKernels<TW, TKV, TM>::attention_rows(hipStream_t st, int n_rows, const float* q, const TKV* kv,
                                                 KvLayout L, int layer, const int* page_table, const int* row_stream,
                                                 const int* row_pos, int hq, int hkv, float* o32, TM* oM) {
-  k_attn_rows<TKV, TM><<<dim3(hq, n_rows), 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, hkv,
-                                                         o32, oM);
+  const dim3 grid(hkv, n_rows);
+  switch (hq / hkv) {
+    case 1: k_attn_rows<TKV, TM, 1><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
+    case 2: k_attn_rows<TKV, TM, 2><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
+    case 4: k_attn_rows<TKV, TM, 4><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
+    default: k_attn_rows<TKV, TM, 8><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
+  }
 }
 
 template <typename TW, typename TKV, typename TM>

@@ -48,10 +48,12 @@ bool config_supported(const hh_config& c, std::string& why) {
   }
   if (c.head_dim != 64) { why = "head_dim must be 64"; return false; }
   if (c.page_size != kPage) { why = "page_size must be 16"; return false; }
-  if (c.n_heads % c.n_kv_heads != 0 || c.n_heads / c.n_kv_heads > 8) {
-    why = "n_heads must be a multiple of n_kv_heads, at most 8 per group";
+  const int grp = c.n_heads / c.n_kv_heads;
+  if (c.n_heads % c.n_kv_heads != 0 || (grp != 1 && grp != 2 && grp != 4 && grp != 8)) {
+    why = "n_heads / n_kv_heads must be 1, 2, 4 or 8";
     return false;
   }
+  if (c.max_context > 32768) { why = "max_context must be at most 32768"; return false; }
   if (c.d_model % 64 != 0) { why = "d_model must be a multiple of 64"; return false; }
   if (c.ffn_dim % 8 != 0) { why = "ffn_dim must be a multiple of 8"; return false; }
   if (c.d_model > 16384 || c.ffn_dim > 65536 || c.n_heads * 64 > 16384) { why = "dimension too large"; return false; }

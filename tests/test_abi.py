@@ -43,6 +43,7 @@ def test_workspace_sizes():
     ("ffn_dim", 690, hh.HH_ERR_UNSUPPORTED),
     ("dtype", 7, hh.HH_ERR_UNSUPPORTED),
     ("max_streams", 0, hh.HH_ERR_UNSUPPORTED),
+    ("max_context", 32769, hh.HH_ERR_UNSUPPORTED),
 ])
 def test_unsupported_configs(field, value, status):
     cfg = hh.make_config(synth.TINY, 2, 128)
@@ -50,6 +51,14 @@ def test_unsupported_configs(field, value, status):
     with pytest.raises(hh.HHError) as e:
         hh.hh_workspace_size(cfg)
     assert e.value.status == status
+
+
+def test_query_group_must_be_power_of_two():
+    cfg = hh.make_config(synth.TINY, 2, 128)
+    cfg.n_heads, cfg.n_kv_heads, cfg.d_model = 12, 4, 768  # 3 query heads per kv head
+    with pytest.raises(hh.HHError) as e:
+        hh.hh_workspace_size(cfg)
+    assert e.value.status == hh.HH_ERR_UNSUPPORTED
 
 
 def test_create_rejects_null_arena_and_small_arena():
