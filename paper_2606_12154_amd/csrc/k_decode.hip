@@ -398,7 +398,12 @@ __global__ __launch_bounds__(256) void k_attn(const float* __restrict__ q, const
       l = l * alpha + wave_sum(quarter == 0 ? p : 0.f);
       o *= alpha;
 #pragma unroll
-      for (int kk = 0; kk < kPage; ++kk) o = fmaf(__shfl(p, kk * 4, kWave), (float)Vp[kk * 64 + lane], o);
+      for (int kk = 0; kk < kPage; ++kk) {
+        // Slots past the stream's length hold stale data (possibly non-finite
+        // bit patterns): their weight is 0, and 0 * NaN would be NaN.
+        const float v = pg * kPage + kk < t ? (float)Vp[kk * 64 + lane] : 0.f;
+        o = fmaf(__shfl(p, kk * 4, kWave), v, o);
+      }
       m = mn;
     }
     if (s_max == 1) {
@@ -503,6 +508,10 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       widen16(P.v[c], vf + c * Vec16<TKV>::n, TKV());
     }
     const bool valid = pg * kPage + key < t;
+    // Slots past the stream's length hold stale data (possibly non-finite bit
+    // patterns): their weight is 0, and 0 * NaN would be NaN.
+#pragma unroll
+    for (int e = 0; e < 16; ++e) vf[e] = valid ? vf[e] : 0.f;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       float a0 = 0.f, a1 = 0.f;

@@ -486,7 +486,11 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
           for (int e = 0; e < 16; ++e) sc = fmaf(qv[e], kf[e], sc);
           sc += dpp<0xB1>(sc);  // the 4 lanes of a key hold quarters of its dot product
           sc += dpp<0x4E>(sc);
-          if (pg * kPage + key >= t) sc = -INFINITY;
+          if (pg * kPage + key >= t) {  // a slot past the length: stale data, weight 0 (and 0 * NaN is NaN)
+            sc = -INFINITY;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) vf[e] = 0.f;
+          }
           const float mn = fmaxf(m, wave_max_u(sc));
           const float alpha = exp2f(m - mn);
           const float pk = exp2f(sc - mn);

@@ -151,3 +151,37 @@ def test_reset_and_errors(tiny):
     ref, _ = model.prefill(toks[:10])
     _, got = ctx.prefill(0, toks[:10], logits="all")
     check_logits(got, ref, TOL, what="after reset")
+
+
+def test_stale_arena_contents(tiny):
+    """The arena is caller memory with arbitrary contents: KV slots past a
+    stream's length (the rest of its last page) must not leak into the
+    result even when they hold non-finite bit patterns.  An allocation of
+    the arena's size is filled with 0xFF bytes (NaN in fp16 and fp32) and
+    released, so torch's caching allocator hands that block to the next
+    context."""
+    import torch
+    from paper_2606_12154_amd import hh
+    shape, tensors, model = tiny
+    cfg = hh.make_config(shape, 4, 96)
+    junk = torch.full((hh.hh_workspace_size(cfg),), 0xFF, dtype=torch.uint8, device="cuda:0")
+    torch.cuda.synchronize()
+    del junk
+    ctx = hh.Context(cfg)
+    try:
+        ctx.load_weights(tensors)
+        lens = [5, 17, 1, 30]  # partial last pages
+        prompts = [synth.make_tokens(shape.vocab, n, 40 + i) for i, n in enumerate(lens)]
+        caches = []
+        for i, p in enumerate(prompts):
+            _, lg = ctx.prefill(i, p, logits="last")
+            ref, cache = model.prefill(p, rows="last")
+            check_logits(lg, ref[0], TOL, what=f"prefill {i}")
+            caches.append(cache)
+        feed = np.array([3, 1000, 2047, 7], np.int32)
+        _, lg = ctx.decode_step([0, 1, 2, 3], feed, logits=True)
+        check_logits(lg, model.decode_batch(caches, feed), TOL, what="multi decode")
+        _, lg = ctx.decode_step([2], [11], logits=True)  # batch-1 kernel on the 1-token stream
+        check_logits(lg[0], model.decode(caches[2], 11), TOL, what="single decode")
+    finally:
+        ctx.close()
