@@ -59,7 +59,8 @@ void flash_prefill(hipStream_t st, const _Float16* qM, const _Float16* kv, KvLay
 constexpr int kStepThreads = 512;     // threads per workgroup (8 waves)
 constexpr int kStepResFloats = 1024;  // LDS row results per workgroup and phase
 constexpr int kStepMaxLayers = 63;    // layers the persistent kernel supports
-constexpr int kStepMaxItemPages = 2048;  // KV pages of one attention item (32768 positions)
+constexpr int kStepRingSlots = 12;    // 8 KiB slots of the per-workgroup LDS weight ring
+constexpr int kStepLoadDepth = 2;    // ring slots each streaming wave keeps in flight (1 .. 7)
 
 template <typename TW>
 struct LayerPtrs {
@@ -67,13 +68,17 @@ struct LayerPtrs {
   const TW* wo;     // [d, Hq * 64]
   const TW* wgu;    // [2F, d] = [Wgate; Wup]
   const TW* wdown;  // [d, F]
+  const TW* wdownT; // [F, d] = Wdown^T (the batch-1 decode kernel's split-K down projection)
   const float* attn_norm;
   const float* mlp_norm;
 };
 
 template <typename TW, typename TKV>
 struct StepParams {
-  int d, F, hq, hkv, V, n_layers, max_ctx, stream, stage_floats;
+  int d, F, hq, hkv, V, n_layers, max_ctx, stream;
+  int ring_slots;              // LDS ring slots per workgroup (<= 16)
+  int load_depth;              // ring slots each streaming wave keeps in flight (1 .. 7)
+  int quiet;                   // 1: streaming pauses while compute waves wait for other workgroups
   float eps;
   unsigned epoch;              // base epoch of this step (distinct for every step)
   const LayerPtrs<TW>* layer;  // device array [n_layers]
@@ -97,7 +102,7 @@ struct StepParams {
   unsigned long long* ll_vn;    // [Hkv * 64] value of the current position
   unsigned long long* ll_part;  // [Hq][nwg / Hkv][66] attention split partials
   unsigned long long* ll_o;     // [Hq * 64] attention output
-  unsigned long long* ll_m;     // [F] SwiGLU output
+  unsigned long long* ll_dp;    // [nwg][d] each workgroup's partial down projection
   unsigned long long* ll_keys;  // [2 * nwg] per-workgroup argmax keys
   int* err;                     // set to 1 if a wait timed out
   unsigned long long* trace;    // nullptr, or [nwg][n_layers + 1][32] phase timestamps
@@ -107,13 +112,17 @@ template <typename TW, typename TKV>
 struct StepKernel {
   static bool supports(int d, int F, int hq, int hkv, int V, int n_layers, int nwg);
   static hipError_t launch(const StepParams<TW, TKV>& P, int nwg, hipStream_t st);
-  static int max_blocks_per_cu(int d, int F, int hq);
-  static size_t lds_bytes(int d, int F, int hq);
+  static int max_blocks_per_cu(int d, int F, int hq, int hkv);
+  static size_t lds_bytes(int d, int F, int hq, int hkv, int ring_slots);
+  static int xc_floats(int d, int F, int hq, int hkv);
 };
 
 // Load-time weight preparation.
 void widen_bf16(hipStream_t st, const __bf16* src, float* dst, size_t n);
 void absmax_bf16(hipStream_t st, const __bf16* src, size_t n, unsigned int* out_bits);
 void bf16_to_f16_scaled(hipStream_t st, const __bf16* src, _Float16* dst, size_t n, float scale);
+// dst = src^T for a row-major rows x cols matrix.
+template <typename T>
+void transpose(hipStream_t st, const T* src, T* dst, int rows, int cols);
 
 }  // namespace hh

@@ -28,6 +28,23 @@ __global__ void k_bf16_to_f16_scaled(const __bf16* __restrict__ src, _Float16* _
     dst[i] = (_Float16)((float)src[i] * scale);
 }
 
+// dst[c][r] = src[r][c] for a rows x cols matrix, through 32 x 32 LDS tiles.
+template <typename T>
+__global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ src, T* __restrict__ dst, int rows, int cols) {
+  __shared__ T tile[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int i = ty; i < 32; i += 8) {
+    const int r = r0 + i, c = c0 + tx;
+    if (r < rows && c < cols) tile[i][tx] = src[(size_t)r * cols + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 32; i += 8) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) dst[(size_t)c * rows + r] = tile[tx][i];
+  }
+}
+
 static int grid_for(size_t n) {
   const size_t b = (n + 255) / 256;
   return (int)(b < 4096 ? (b > 0 ? b : 1) : 4096);
@@ -42,5 +59,13 @@ void absmax_bf16(hipStream_t st, const __bf16* src, size_t n, unsigned int* out_
 void bf16_to_f16_scaled(hipStream_t st, const __bf16* src, _Float16* dst, size_t n, float scale) {
   k_bf16_to_f16_scaled<<<grid_for(n), 256, 0, st>>>(src, dst, n, scale);
 }
+
+template <typename T>
+void transpose(hipStream_t st, const T* src, T* dst, int rows, int cols) {
+  dim3 grid((cols + 31) / 32, (rows + 31) / 32);
+  k_transpose<T><<<grid, 256, 0, st>>>(src, dst, rows, cols);
+}
+template void transpose<__bf16>(hipStream_t, const __bf16*, __bf16*, int, int);
+template void transpose<float>(hipStream_t, const float*, float*, int, int);
 
 }  // namespace hh

@@ -1,34 +1,149 @@
 // Batch-1 decode step as ONE persistent kernel for gfx950.
 //
 // One 512-thread workgroup per CU runs the whole token: embedding, then per
-// layer the fused RMSNorm+QKV+RoPE+KV-append phase, paged GQA attention
-// (split over pages; split 0 of each kv head combines), O projection +
-// residual, RMSNorm+gate/up+SwiGLU, down projection + residual, and finally
-// RMSNorm + LM head + argmax, reduced by workgroup 0 which publishes the token.
+// layer RMSNorm + QKV + RoPE + KV append, paged GQA attention, O projection +
+// residual, RMSNorm + gate/up + SwiGLU, down projection + residual, and
+// finally RMSNorm + LM head + argmax, reduced by workgroup 0 which publishes
+// the token.
 //
-// Batch-1 decode is bound by reading every weight once from HBM.  Each phase
-// splits its weight rows evenly over the workgroups; a wave owns whole rows and
-// streams them with coalesced 16-byte non-temporal loads (a wave instruction
-// reads 1 KiB of a row), double-buffered in registers, with the fp32 input
-// vector staged in LDS.  Each output row is produced by exactly one wave, so
-// results are bitwise reproducible.
+// Batch-1 decode is bound by reading every weight once from HBM, but its
+// phases are chained: every phase needs the whole output of the phase before,
+// computed by all CUs.  The kernel therefore separates streaming from
+// computing inside each workgroup:
+//
+//  * wave 0 (the streaming wave) walks the workgroup's whole byte stream for
+//    the token -- its rows of every weight matrix, layer by layer, plus the
+//    K/V pages of its attention item -- and copies it with direct global->LDS
+//    loads into a ring of 8 KiB slots.  It keeps only a few slots in flight
+//    (enough to saturate HBM, few enough that the memory queues stay short),
+//    and it never waits for activations: it only waits for free ring slots.
+//  * waves 1..7 (compute waves) wait for a phase's input vector, then consume
+//    the phase's ring slots (dot products of staged rows with the input, or
+//    attention over staged K/V pages), and publish the phase's outputs.
+//
+// While compute waves wait for other CUs at a phase boundary, the streaming
+// wave keeps filling the ring with the next phases' weights, so HBM stays busy
+// through the exchange latency instead of idling.
 //
 // Workgroups exchange activations without grid barriers or memory fences:
 // every value crossing workgroups travels as one 64-bit word (fp32 bits | a
 // 32-bit epoch naming the step, layer and phase), written with a single
 // relaxed agent-scope store, so a reader that sees the expected epoch also
-// sees the value.  A consumer polls exactly the words it needs.  On this chip
-// an agent-scope fence (an L2 write-back/invalidate) costs several
-// microseconds while a flag crosses CUs in about half a microsecond, so this
-// turns each phase boundary into one flag latency.  Because weights do not
-// depend on activations, every wave issues its first batch of a phase's weight
-// loads BEFORE polling that phase's input, so the wait overlaps HBM streaming.
+// sees the value.  Inside a workgroup, the streaming and compute waves
+// synchronise through LDS counters (slots landed, slots consumed, a barrier
+// among compute waves); every wait is bounded in time and gives up through a
+// shared error flag, so every wave always terminates.
+//
+// Attention: an item is one kv head over a range of pages (all query heads of
+// the group together, so K/V are read once).  For fp16 K/V the scores and the
+// weighted sum use 16x16x32 fp16 MFMAs (queries split into fp16 high and low
+// parts, so the scores keep fp32 accuracy); fp32 K/V use the VALU.  Items of
+// at most two splits per kv head are combined by the consumers while they
+// stage the O-projection input; longer contexts combine in split 0's
+// workgroup.
 #include "hh_kernels.h"
 
 namespace hh {
 
-constexpr int kStepWaves = kStepThreads / 64;
-constexpr unsigned kSpinLimit = 1u << 20;  // polls (~1 s) before a wait gives up
+constexpr int kWaves = kStepThreads / 64;  // 8
+constexpr int kLoaders = 3;                // streaming waves (one wave's direct-to-LDS loads top out near 13 GB/s)
+constexpr int kNC = kWaves - kLoaders;     // compute waves
+// Poll widths (words per compute thread) that cover the 1B shapes in one round.
+constexpr int kPollX = (2048 + 64 * kNC - 1) / (64 * kNC);
+constexpr int kHeadsPerWave = (32 + kNC - 1) / kNC;
+constexpr int kSlot = 8192;                // ring slot: 8 pieces of 1 KiB
+constexpr int kMaxRing = 16;               // ring slots supported
+constexpr int kItemKvBytes = 64 * 1024;    // K/V bytes aimed at per attention item
+constexpr int kMaxItemPages = 256;         // pages of one attention item
+constexpr int kMaxConsumerSplits = 2;      // splits per kv head merged by the O-phase consumers
+constexpr int kMaxGroup = 8;               // query heads per kv head (fp16 K/V)
+constexpr int kMaxGroupF32 = 4;            // query heads per kv head (fp32 K/V)
+constexpr int kStRow = 68;                 // LDS floats per (wave, head) attention state: m, l, o[64], pad
+constexpr unsigned long long kWaitTicks = 100000000ull;  // 1 s of the 100 MHz real-time clock
+
+typedef _Float16 f16x8v __attribute__((ext_vector_type(8)));
+
+// Explicit address spaces: a generic (flat) access to LDS goes through the
+// vector-memory path and is ordered behind the CU's in-flight global loads,
+// so every LDS flag and every global pointer read from LDS is typed here.
+#define HH_LDS __attribute__((address_space(3)))
+#define HH_GLB __attribute__((address_space(1)))
+
+// Floats of the second staging buffer: the down-projection input [F], or the
+// O-projection input [Hq * 64] followed by the attention states of the
+// compute waves.
+__host__ __device__ constexpr int step_xc_floats(int d, int hq, int hkv) {
+  return (kNC - 1) * d > hq * 64 + kNC * (hq / hkv) * kStRow ? (kNC - 1) * d : hq * 64 + kNC * (hq / hkv) * kStRow;
+}
+
+// ---------------------------------------------------------------- waits
+
+// LDS block shared by the streaming and compute waves.
+struct RingSync {
+  int cbar;      // arrivals at compute-wave barriers
+  int abort;     // set when a wait gave up: every later wait returns at once
+  int quiet;     // compute waves are waiting for another workgroup's outputs
+  int landed[kMaxRing];    // per ring position: stream index of the last slot landed there
+  int consumed[kMaxRing];  // per ring position: stream index of the last slot consumed there
+  float ss[kNC];           // per compute wave: partial sum of squares of a staged vector
+};
+
+// Called in a wait loop: true once the wait must give up (after 1 s, or once
+// any wait of this workgroup or of another one has given up).
+__device__ __forceinline__ bool give_up(unsigned& spins, unsigned long long& t0, RingSync HH_LDS* sy, int HH_GLB* err) {
+  if ((++spins & 63u) != 0) return false;
+  if (*(volatile int HH_LDS*)&sy->abort) return true;
+  const unsigned long long t = wall_clock64();
+  if (t0 == 0) {
+    t0 = t;
+    return false;
+  }
+  if (t - t0 > kWaitTicks || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+    *(volatile int HH_LDS*)&sy->abort = 1;
+    __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+  }
+  return false;
+}
+
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+// s_waitcnt lgkmcnt(0) (vmcnt and expcnt left at their maxima).
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+#define HH_STEP_VMWAIT(c) __builtin_amdgcn_s_waitcnt(((c) & 15) | (0x7 << 4) | (0xF << 8) | (((c) >> 4) << 14))
+
+// Barrier among the compute waves (the streaming wave never joins one).
+__device__ __forceinline__ void cbar(RingSync HH_LDS* sy, int& gen, int HH_GLB* err) {
+  gen += 1;
+  compiler_fence();
+  wait_lds();
+  if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(&sy->cbar, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  unsigned spins = 0;
+  unsigned long long t0 = 0;
+  while (*(volatile int HH_LDS*)&sy->cbar < gen * kNC) {
+    __builtin_amdgcn_s_sleep(1);
+    if (give_up(spins, t0, sy, err)) break;
+  }
+  compiler_fence();
+}
+
+__device__ __forceinline__ void wait_landed(RingSync HH_LDS* sy, int n, int pos, int HH_GLB* err) {
+  if (*(volatile int HH_LDS*)&sy->landed[pos] < n) {
+    unsigned spins = 0;
+    unsigned long long t0 = 0;
+    while (*(volatile int HH_LDS*)&sy->landed[pos] < n) {
+      __builtin_amdgcn_s_sleep(1);
+      if (give_up(spins, t0, sy, err)) break;
+    }
+  }
+  compiler_fence();
+}
+
+// This wave's LDS reads of ring slot n are complete: hand it back.
+__device__ __forceinline__ void release_slot(RingSync HH_LDS* sy, int pos, int n) {
+  compiler_fence();
+  wait_lds();
+  if ((threadIdx.x & 63) == 0) *(volatile int HH_LDS*)&sy->consumed[pos] = n;
+}
 
 // ---------------------------------------------------------------- epoch words
 
@@ -42,103 +157,70 @@ __device__ __forceinline__ void ll_put_u(unsigned long long* p, unsigned v, unsi
 __device__ __forceinline__ unsigned long long ll_get(const unsigned long long* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// Poll word p (first read already in w) until it carries epoch ep; returns
-// its 32-bit payload.  A wait longer than kSpinLimit polls, or any wait after
-// another one timed out, sets *err and returns the stale payload, so every
-// wave always terminates.
-__device__ __forceinline__ unsigned ll_wait(const unsigned long long* p, unsigned ep, unsigned long long w,
-                                            int* err) {
-  unsigned spins = 0;
-  while ((unsigned)(w >> 32) != ep) {
-    __builtin_amdgcn_s_sleep(1);
-    w = ll_get(p);
-    if ((++spins & 255u) == 0) {
-      if (spins > kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
-      }
-    }
-  }
-  return (unsigned)w;
-}
 
-// xs[i] = value of word src[i] at epoch ep for i < n (all threads of the
-// block); returns the block-wide sum of squares.  A thread loads all of its
-// (up to U) words at once and, while any is stale, re-polls only the stale
-// ones together, so a late producer costs one round trip, not one per word.
-__device__ __forceinline__ float ll_stage(const unsigned long long* __restrict__ src, int n, unsigned ep, float* xs,
-                                          float* red, int* err) {
-  constexpr int U = 16;
-  float ss = 0.f;
-  for (int base = threadIdx.x; base < n; base += kStepThreads * U) {
+// Compute-wave threads (index tc = tid - 128 of NT = 384) read the words
+// addr(i), i < n, at epoch ep and pass (i, value) to f.  A thread issues all
+// of its (at most U per round) loads at once and then re-polls only the stale
+// ones, so a late producer costs one more round trip, not one per word.
+// Diagnostic record of one poll (thread 0 of the compute waves): when the
+// first round returned and how many rounds ran.
+struct PollTrace {
+  unsigned long long* rec;  // nullptr, or 2 words: first-return time, rounds
+};
+
+template <int U, class A, class F>
+__device__ __forceinline__ void poll_words(A&& addr, int n, unsigned ep, RingSync HH_LDS* sy, int HH_GLB* err, F&& f,
+                                           PollTrace pt = PollTrace{nullptr}) {
+  constexpr int NT = kNC * 64;
+  const int tc = (int)threadIdx.x - 64 * kLoaders;
+  for (int base = tc; base < n; base += NT * U) {
     unsigned long long w[U];
-    unsigned stale = 0;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int i = base + u * kStepThreads;
-      w[u] = i < n ? ll_get(src + i) : ((unsigned long long)ep << 32);
+      const int i = base + u * NT;
+      w[u] = i < n ? ll_get(addr(i)) : ((unsigned long long)ep << 32);
     }
+    unsigned stale = 0;
 #pragma unroll
     for (int u = 0; u < U; ++u) stale |= ((unsigned)(w[u] >> 32) != ep ? 1u : 0u) << u;
+    if (pt.rec && tc == 0) pt.rec[0] = wall_clock64();
+    unsigned rounds = 1;
     unsigned spins = 0;
+    unsigned long long t0 = 0;
     while (stale) {
+      ++rounds;
       __builtin_amdgcn_s_sleep(1);
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        if (stale & (1u << u)) w[u] = ll_get(src + base + u * kStepThreads);
+        if (stale & (1u << u)) w[u] = ll_get(addr(base + u * NT));
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if ((stale & (1u << u)) && (unsigned)(w[u] >> 32) == ep) stale &= ~(1u << u);
-      if ((++spins & 255u) == 0 && stale) {
-        if (spins > kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-          __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          break;
-        }
-      }
+      if (stale && give_up(spins, t0, sy, err)) break;
     }
+    if (pt.rec && tc == 0) pt.rec[1] = rounds;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int i = base + u * kStepThreads;
-      if (i < n) {
-        const float v = __uint_as_float((unsigned)w[u]);
-        xs[i] = v;
-        ss += v * v;
-      }
+      const int i = base + u * NT;
+      if (i < n) f(i, __uint_as_float((unsigned)w[u]));
     }
   }
-  ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  float tot = 0.f;
-#pragma unroll
-  for (int w = 0; w < kStepWaves; ++w) tot += red[w];
-  __syncthreads();
-  return tot;
+}
+template <int U, class F>
+__device__ __forceinline__ void poll_span(const unsigned long long* __restrict__ src, int n, unsigned ep, RingSync HH_LDS* sy,
+                                          int HH_GLB* err, F&& f, PollTrace pt = PollTrace{nullptr}) {
+  poll_words<U>([=](int i) { return src + i; }, n, ep, sy, err, f, pt);
 }
 
-// In-place RMSNorm of the staged vector: xs *= rsqrt(ss / n + eps) * gain,
-// with this thread's gains (elements tid + 512 k) already in registers.
-template <int NR>
-__device__ __forceinline__ void norm_staged(float* xs, int n, float ss, float eps, const float* gr) {
-  const float inv = rsqrtf(ss / (float)n + eps);
-#pragma unroll
-  for (int k = 0; k < NR; ++k) {
-    const int i = threadIdx.x + k * kStepThreads;
-    if (i < n) xs[i] = xs[i] * inv * gr[k];
-  }
-  __syncthreads();
-}
-
-// ---------------------------------------------------------------- row streaming
+// ---------------------------------------------------------------- row dot products
 
 // Sum RB per-lane partials over the wave.  Returns, in lane l, the total of
 // row l >> (6 - log2 RB); a butterfly halves the row set at each of the first
-// log2 RB exchange steps, so RB rows cost log2 RB + 6 - log2 RB + (RB - 1)
-// shuffles instead of 6 RB.
+// log2 RB exchange steps.
 template <int RB>
 __device__ __forceinline__ float reduce_rows(float* v) {
-  constexpr int LOG = RB == 1 ? 0 : RB == 2 ? 1 : RB == 4 ? 2 : RB == 8 ? 3 : 4;
-  static_assert((1 << LOG) == RB, "RB must be 1, 2, 4, 8 or 16");
+  constexpr int LOG = RB == 1 ? 0 : RB == 2 ? 1 : RB == 4 ? 2 : 3;
+  static_assert((1 << LOG) == RB, "RB must be 1, 2, 4 or 8");
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int s = 0; s < LOG; ++s) {
@@ -160,118 +242,93 @@ __device__ __forceinline__ float reduce_rows(float* v) {
   return r;
 }
 
-constexpr int pow2_floor(int v) { return v >= 16 ? 16 : v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 1; }
+constexpr int rows_per_slot(int np) { return np >= 8 ? 1 : 8 / np; }
+constexpr int log2_small(int v) { return v >= 8 ? 3 : v >= 4 ? 2 : v >= 2 ? 1 : 0; }
 
-// One register batch of a wave: RB rows x CHB 16-byte chunks per lane
-// (RB * CHB <= 8 outstanding loads per lane).  A row has CH chunks per lane
-// (lane l reads chunks l, l + 64, ...), taken in NCB = CH / CHB blocks; batch
-// b covers row group b / NCB and chunk block b % NCB.  Wave w of a workgroup
-// owns the local rows w, w + 8, w + 16, ...; row group g holds its rows
-// g*RB .. g*RB + RB - 1.
-// Registers of one wave's in-flight weight loads: 8 x 16 bytes per lane.
-struct WBuf {
-  u32x4 w[8];
-};
+// Slots of a segment of n rows with np 1 KiB pieces per row: a slot holds
+// 8 / np whole rows (np <= 8) or 8 pieces of one row (np > 8, np % 8 == 0).
+__device__ __forceinline__ int row_slots(int n, int np) {
+  return np <= 8 ? (n + (8 / np) - 1) / (8 / np) : n * (np / 8);
+}
 
-// View of a WBuf for rows of CH chunks per lane: RB rows x CHB chunks
-// (RB * CHB = 8, RB a power of two).  A row's CH chunks (lane l reads chunks
-// l, l + 64, ...) are taken in NCB = CH / CHB blocks; batch b covers row group
-// b / NCB and chunk block b % NCB.  Wave w of a workgroup owns the local rows
-// w, w + 8, w + 16, ...; row group g holds its rows g*RB .. g*RB + RB - 1.
-template <typename TW, int CH>
-struct RowBatch {
-  static constexpr int CHB = CH >= 8 ? 8 : CH;
-  static constexpr int NCB = CH / CHB;
-  static constexpr int RB = pow2_floor(8 / CHB);
-  static constexpr int LOG = RB == 1 ? 0 : RB == 2 ? 1 : RB == 4 ? 2 : RB == 8 ? 3 : 4;
-  static_assert(CH % CHB == 0, "chunk blocks must tile the row");
-  static_assert(RB * CHB <= 8, "batch exceeds the register buffer");
-
-  template <class Map>
-  static __device__ __forceinline__ void issue(WBuf& B, const TW* __restrict__ W, int K, const Map& map, int n_local,
-                                               int b) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nch = K / Vec16<TW>::n;
-    const int grp = b / NCB, cb = b % NCB;
+// One ring slot of weight rows (slot index k of its segment) against the
+// staged fp32 vector xs of K elements.  Lane l reads the 16 bytes at offset
+// 16 l of every piece.  NP <= 8: writes res[row] for the slot's rows; NP > 8:
+// writes the partial res[row * (NP / 8) + chunk].  FULL: K fills the pieces
+// exactly, so every read is issued up front with no per-piece branch (rows
+// missing from the slot hold a copy of its first row and are read but not
+// written back).
+template <typename TW, int NP, bool FULL>
+__device__ __forceinline__ void slot_rows(const char* slot, const float* xs, int K, int k, int n_rows, float* res) {
+  constexpr int E = 16 / (int)sizeof(TW);     // elements per lane per piece
+  constexpr int PE = 1024 / (int)sizeof(TW);  // elements per piece
+  const int lane = threadIdx.x & 63;
+  if constexpr (NP <= 8) {
+    constexpr int RPS = rows_per_slot(NP);
+    constexpr int LOG = log2_small(RPS);
+    static_assert((1 << LOG) == RPS, "rows per slot must be a power of two");
+    const int r0 = k * RPS;
+    float acc[RPS];
 #pragma unroll
-    for (int r = 0; r < RB; ++r) {
-      const int lr = wave + kStepWaves * (grp * RB + r);
-      const int row = lr < n_local ? map(lr) : -1;
-      const u32x4* src = reinterpret_cast<const u32x4*>(W + (size_t)(row < 0 ? 0 : row) * K);
+    for (int r = 0; r < RPS; ++r) acc[r] = 0.f;
 #pragma unroll
-      for (int c = 0; c < CHB; ++c) {
-        const int ch = lane + 64 * (cb * CHB + c);
-        if (row >= 0 && ch < nch) B.w[r * CHB + c] = __builtin_nontemporal_load(src + ch);
-        else B.w[r * CHB + c] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  }
-
-  // Accumulate the batch's dot products with the LDS vector xs into acc; on
-  // the row group's last chunk block, reduce and store res[lr] = row total.
-  static __device__ __forceinline__ void consume(const WBuf& B, const float* xs, int K, int n_local, int b,
-                                                 float* acc, float* res) {
-    constexpr int V = Vec16<TW>::n;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nch = K / V;
-    const int grp = b / NCB, cb = b % NCB;
+    for (int c = 0; c < NP; ++c) {
+      const int e0 = c * PE + lane * E;
+      const bool ok = FULL || e0 < K;
+      float xv[E];
 #pragma unroll
-    for (int c = 0; c < CHB; ++c) {
-      const int ch = lane + 64 * (cb * CHB + c);
-      if (ch < nch) {
-        float xv[V];
-#pragma unroll
-        for (int e = 0; e < V; e += 4) {
-          const float4 t = *reinterpret_cast<const float4*>(xs + ch * V + e);
-          xv[e] = t.x;
-          xv[e + 1] = t.y;
-          xv[e + 2] = t.z;
-          xv[e + 3] = t.w;
-        }
-#pragma unroll
-        for (int r = 0; r < RB; ++r) {
-          float wf[V];
-          widen16(B.w[r * CHB + c], wf, TW());
-#pragma unroll
-          for (int e = 0; e < V; ++e) acc[r] = fmaf(wf[e], xv[e], acc[r]);
-        }
-      }
-    }
-    if (cb == NCB - 1) {
-      const float tot = reduce_rows<RB>(acc);
-      const int r = lane >> (6 - LOG);
-      if ((lane & ((64 >> LOG) - 1)) == 0) {
-        const int lr = wave + kStepWaves * (grp * RB + r);
-        if (lr < n_local) res[lr] = tot;
+      for (int e = 0; e < E; e += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(xs + e0 + e);
+        xv[e] = ok ? t.x : 0.f;
+        xv[e + 1] = ok ? t.y : 0.f;
+        xv[e + 2] = ok ? t.z : 0.f;
+        xv[e + 3] = ok ? t.w : 0.f;
       }
 #pragma unroll
-      for (int i = 0; i < RB; ++i) acc[i] = 0.f;
-    }
-  }
-};
-
-// Stream the workgroup's n_local rows; `cur` already holds batch 0.
-template <typename TW, int CH, class Map>
-__device__ __forceinline__ void run_rows(WBuf& cur, const TW* __restrict__ W, int K, const Map& map, int n_local,
-                                         const float* xs, float* res) {
-  using B = RowBatch<TW, CH>;
-  const int per_wave = (n_local + kStepWaves - 1) / kStepWaves;
-  const int nb = (per_wave + B::RB - 1) / B::RB * B::NCB;
-  float acc[B::RB];
+      for (int r = 0; r < RPS; ++r) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(slot + (r * NP + c) * 1024 + lane * 16);
+        float wf[E];
+        widen16(w, wf, TW());
 #pragma unroll
-  for (int i = 0; i < B::RB; ++i) acc[i] = 0.f;
-  WBuf nxt;
-  for (int b = 0; b < nb; ++b) {
-    if (b + 1 < nb) B::issue(nxt, W, K, map, n_local, b + 1);
-    B::consume(cur, xs, K, n_local, b, acc, res);
-    cur = nxt;
+        for (int e = 0; e < E; ++e) acc[r] = fmaf(ok ? wf[e] : 0.f, xv[e], acc[r]);
+      }
+    }
+    // Row totals by DPP row sums and lane reads (VALU only: a chain of
+    // LDS-routed shuffles would dominate the latency of a small phase).
+#pragma unroll
+    for (int r = 0; r < RPS; ++r) {
+      const float tot = wave_sum_u(acc[r]);
+      if (lane == 0 && r0 + r < n_rows) res[r0 + r] = tot;
+    }
+  } else {
+    static_assert(NP % 8 == 0, "long rows must be whole slots");
+    constexpr int CPR = NP / 8;
+    const int row = k / CPR, ch = k % CPR;
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int e0 = (ch * 8 + c) * PE + lane * E;
+      const bool ok = FULL || e0 < K;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(slot + c * 1024 + lane * 16);
+      float wf[E];
+      widen16(w, wf, TW());
+#pragma unroll
+      for (int e = 0; e < E; e += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(xs + e0 + e);
+        acc = fmaf(ok ? wf[e] : 0.f, ok ? t.x : 0.f, acc);
+        acc = fmaf(ok ? wf[e + 1] : 0.f, ok ? t.y : 0.f, acc);
+        acc = fmaf(ok ? wf[e + 2] : 0.f, ok ? t.z : 0.f, acc);
+        acc = fmaf(ok ? wf[e + 3] : 0.f, ok ? t.w : 0.f, acc);
+      }
+    }
+    acc = wave_sum_u(acc);
+    if (lane == 0 && row < n_rows) res[row * CPR + ch] = acc;
   }
 }
 
-// ---------------------------------------------------------------- row maps
+// ---------------------------------------------------------------- the plan
 
 // Weight rows of a GEMV phase as a function of the workgroup-local row index.
-// One map type for every phase keeps a single copy of the streaming code.
 struct RowMap {
   int mode;  // 0: r0 + lr; 1: rotary pairs from pair r0; 2: gate/up outputs from r0
   int r0, nj, F;
@@ -290,404 +347,429 @@ __device__ __forceinline__ void split_range(int n, int parts, int i, int& b, int
   e = (int)(((long long)n * (i + 1)) / parts);
 }
 
+enum : int { SG_QKV = 0, SG_KV = 1, SG_O = 2, SG_GU = 3, SG_DOWN = 4, SG_HEAD = 5 };
+
+// The workgroup's share of the step (identical arithmetic in every wave).
+struct Plan {
+  int pq0, pq1;  // rotary pairs of [Wq; Wk; Wv]
+  int rd0, rd1;  // rows of Wo / Wdown / x
+  int j0, j1;    // SwiGLU outputs (gate and up rows)
+  int v0, v1;    // LM head rows
+  // attention: items are (kv head, split) on workgroups 0 .. n_items - 1
+  int nspl, pps, n_items, has_item, it_g, it_sp, it_pg0, it_pg1, consumer_comb;
+  // Ring slots per layer of each segment, and the segment's first slot
+  // within the layer (named fields: an array indexed at run time would live
+  // in scratch memory).
+  int n_qkv, n_kv, n_o, n_gu, n_down;
+  int o_qkv, o_kv, o_o, o_gu, o_down;
+  int per_layer, head_slots;
+  __device__ __forceinline__ int slots(int sg) const {
+    switch (sg) {
+      case SG_QKV: return n_qkv;
+      case SG_KV: return n_kv;
+      case SG_O: return n_o;
+      case SG_GU: return n_gu;
+      case SG_DOWN: return n_down;
+      default: return head_slots;
+    }
+  }
+};
+
+template <typename TW, typename TKV, int NPD>
+__device__ __forceinline__ void make_plan(Plan& pl, const StepParams<TW, TKV>& P, int wg, int nwg, int t) {
+  const int d = P.d, F = P.F, hq = P.hq, hkv = P.hkv;
+  split_range((hq + 2 * hkv) * 32, nwg, wg, pl.pq0, pl.pq1);
+  split_range(d, nwg, wg, pl.rd0, pl.rd1);
+  split_range(P.V, nwg, wg, pl.v0, pl.v1);
+  // Attention items: split the t positions' pages so an item streams about
+  // kItemKvBytes of K/V.
+  constexpr int page_bytes = 2 * kPage * 64 * (int)sizeof(TKV);  // K and V of one page, one kv head
+  constexpr int pps = kSlot / page_bytes;                          // pages per ring slot
+  const int npg = (t + kPage - 1) / kPage;
+  const int cap = kItemKvBytes / page_bytes;
+  const int s_cap = nwg / hkv;
+  int nspl = (npg + cap - 1) / cap;
+  nspl = nspl < s_cap ? nspl : s_cap;
+  int per = (npg + nspl - 1) / nspl;
+  nspl = (npg + per - 1) / per;
+  pl.nspl = nspl;
+  pl.pps = pps;
+  pl.n_items = hkv * nspl;
+  pl.has_item = wg < pl.n_items;
+  pl.it_g = wg / nspl;
+  pl.it_sp = wg % nspl;
+  pl.it_pg0 = pl.it_sp * per;
+  pl.it_pg1 = pl.it_pg0 + per < npg ? pl.it_pg0 + per : npg;
+  pl.consumer_comb = nspl <= kMaxConsumerSplits;
+  // SwiGLU outputs: item workgroups take fewer, so every workgroup streams
+  // about the same bytes per layer.  A gate/up output is two d-rows.
+  const int kv_slots = (per + pps - 1) / pps;
+  const int gu_unit = 2 * NPD * 1024;  // bytes of one output's rows
+  int kvu = (kv_slots * kSlot + gu_unit / 2) / gu_unit;
+  long long tot = (long long)F + (long long)pl.n_items * kvu;
+  if (tot < (long long)kvu * nwg) {  // items would get a negative share: plain split
+    kvu = 0;
+    tot = F;
+  }
+  auto cum = [&](int w) -> int {
+    const int wi = w < pl.n_items ? w : pl.n_items;
+    return (int)(((long long)w * tot - (long long)wi * kvu * nwg) / nwg);
+  };
+  pl.j0 = cum(wg);
+  pl.j1 = cum(wg + 1);
+  pl.n_qkv = row_slots(2 * (pl.pq1 - pl.pq0), NPD);
+  pl.n_kv = pl.has_item ? (pl.it_pg1 - pl.it_pg0 + pps - 1) / pps : 0;
+  pl.n_o = row_slots(pl.rd1 - pl.rd0, NPD);
+  pl.n_gu = row_slots(2 * (pl.j1 - pl.j0), NPD);
+  pl.n_down = row_slots(pl.j1 - pl.j0, NPD);
+  pl.o_qkv = 0;
+  pl.o_kv = pl.n_qkv;
+  pl.o_o = pl.o_kv + pl.n_kv;
+  pl.o_gu = pl.o_o + pl.n_o;
+  pl.o_down = pl.o_gu + pl.n_gu;
+  pl.per_layer = pl.o_down + pl.n_down;
+  pl.head_slots = row_slots(pl.v1 - pl.v0, NPD);
+}
+
+// ---------------------------------------------------------------- streaming
+
+// Issue the 8 direct global->LDS loads (1 KiB each, lane l: 16 bytes at
+// 16 l) of ring slot k of a row segment: 8 / NP whole rows (NP <= 8, rows
+// missing at the end repeat the slot's first row; pieces beyond 8 / NP * NP
+// repeat its first piece) or 8 pieces of one row (NP > 8).  full: rows are a
+// whole number of pieces (no lane reads past the end of a row).
+template <int NP>
+__device__ __forceinline__ void issue_row_slot(char* dst, const char* W, const RowMap& map, int rowb, int nrows, int k,
+                                               bool full) {
+  const int lane = threadIdx.x & 63;
+  if constexpr (NP <= 8) {
+    constexpr int RPS = rows_per_slot(NP);
+    const int lr0 = k * RPS;
+    const char* first = W + (size_t)map(lr0) * rowb;
+#pragma unroll
+    for (int r = 0; r < RPS; ++r) {
+      const char* row = r == 0 ? first : lr0 + r < nrows ? W + (size_t)map(lr0 + r) * rowb : first;
+#pragma unroll
+      for (int c = 0; c < NP; ++c) {
+        int off = c * 1024 + lane * 16;
+        if (!full && off + 16 > rowb) off = 0;
+        __builtin_amdgcn_global_load_lds(row + off, dst + (r * NP + c) * 1024, 16, 0, 2);
+      }
+    }
+#pragma unroll
+    for (int q = RPS * NP; q < 8; ++q) __builtin_amdgcn_global_load_lds(first, dst + q * 1024, 16, 0, 2);
+  } else {
+    constexpr int CPR = NP / 8;
+    const int row = k / CPR, ch = k - row * CPR;
+    const char* src = W + (size_t)map(row) * rowb + ch * 8 * 1024;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      int off = q * 1024 + lane * 16;
+      if (!full && ch * 8 * 1024 + off + 16 > rowb) off = 0;
+      __builtin_amdgcn_global_load_lds(src + off, dst + q * 1024, 16, 0, 2);
+    }
+  }
+}
 
 // ---------------------------------------------------------------- kernel
 
-// Optional phase timestamps (100 MHz s_memrealtime), one row per workgroup.
+// Optional timestamps (100 MHz s_memrealtime), [workgroup][layer][32 events].
 #define STEP_MARK(l, ev)                                                                           \
   do {                                                                                             \
-    if (P.trace && tid == 0) P.trace[((size_t)wg * (L + 1) + (l)) * 32 + (ev)] = wall_clock64();   \
+    if (P.trace && threadIdx.x == 64 * kLoaders) P.trace[((size_t)wg * (L + 1) + (l)) * 32 + (ev)] = wall_clock64(); \
   } while (0)
 
 // Epoch of (layer, phase) in this step; phases: 0 q/k/v, 1 attention
-// partials, 2 attention output, 3 x after O, 4 SwiGLU output, 5 x after down,
-// 6 argmax keys.  The layer field is 6 bits wide (at most 63 layers + head).
+// partials, 2 combined attention output, 3 x after O, 4 SwiGLU output, 5 x
+// after down, 6 argmax keys.  The layer field is 6 bits wide.
 __device__ __forceinline__ unsigned ep_of(unsigned base, int l, int ph) { return base + (unsigned)l * 8u + ph; }
 
-enum : int { PH_QKV = 0, PH_O = 1, PH_GU = 2, PH_DOWN = 3, PH_HEAD = 4 };
-constexpr int kKvStageBytes = 72 * 1024;  // LDS holding an attention item's K/V pages
-constexpr int kNormRegs = 8;              // gain values per thread (d <= 8 * 512)
-constexpr int kMaxSplitsPerWave = 8;  // split partials one combiner wave loads per round
-
-template <typename TW, typename TKV, int CHD, int CHF>
+template <typename TW, typename TKV, int NPD, bool FD>
 __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV> P) {
-  extern __shared__ float smem[];
-  float* xs = smem;                      // [stage_floats] staged input vector
-  float* res = xs + P.stage_floats;      // [kStepResFloats] row results
-  float* st = res + kStepResFloats;      // [8 waves][4 rows][66] attention states
-  float* qs = st + kStepWaves * 4 * 66;  // [8][64] query heads of a kv group
-  float* kn = qs + kStepWaves * 64;      // [64] key of the current position
-  float* vn = kn + 64;                   // [64] value of the current position
-  float* xown = vn + 64;                 // [kStepResFloats] this workgroup's rows of x
-  TKV* kvs = reinterpret_cast<TKV*>(xown + kStepResFloats);  // [pages][K|V][16][64] staged K/V
-  __shared__ float red[kStepWaves];
-  __shared__ unsigned long long kred[kStepWaves];
-  __shared__ float2 rope_p[32];  // cos/sin of this step's position
-  __shared__ LayerPtrs<TW> lptr[kStepMaxLayers];  // per-layer weight pointers
-  __shared__ int item_pages[kStepMaxItemPages];   // physical pages of this workgroup's attention item
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ RingSync sy;
+  RingSync HH_LDS* const syp = (RingSync HH_LDS*)&sy;
+  __shared__ float2 rope_p[32];                    // cos/sin of this step's position
+  __shared__ LayerPtrs<TW> lptr[kStepMaxLayers];   // per-layer weight pointers
+  __shared__ int item_pages[kMaxItemPages];        // physical pages of this workgroup's attention item
+  __shared__ float qs[kMaxGroup * 64];             // the item's query heads, pre-scaled
+  __shared__ float kn[64], vn[64];                 // key / value of the current position (kv head of the item)
+  __shared__ unsigned long long kred[kNC];
 
   const int wg = blockIdx.x, nwg = gridDim.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = P.d, F = P.F, hq = P.hq, hkv = P.hkv, G = hq / hkv, L = P.n_layers;
+  const int S = P.ring_slots;
   const int s = P.stream;
   const int p = P.pos[s];
   const int tok = P.feed ? P.feed[0] : P.pending[s];
   const int t = p + 1;  // keys attended this step
   const unsigned E0 = P.epoch;
-
-  int pq0, pq1, rd0, rd1, j0, j1, v0, v1;
-  split_range((hq + 2 * hkv) * 32, nwg, wg, pq0, pq1);  // rotary pairs of [Wq; Wk; Wv]
-  split_range(d, nwg, wg, rd0, rd1);                     // rows of Wo / Wdown / x
-  split_range(F, nwg, wg, j0, j1);                       // SwiGLU outputs
-  split_range(P.V, nwg, wg, v0, v1);                     // LM head rows
-  const int nd = rd1 - rd0;
-
-  // Attention plan (identical in every workgroup).  An item is a set of nh
-  // query heads of kv head g over the pages of split sp; its K/V pages are
-  // staged in LDS (at most kv_cap per stage).  Short contexts use one item
-  // per query head (nh = 1, all waves split the pages, no combine step);
-  // long ones use items per kv head (nh = G) split over up to nwg / Hkv
-  // workgroups, whose partials the item of split 0 combines.
-  const int npg = (t + kPage - 1) / kPage;
-  const int kv_cap = kKvStageBytes / (2 * kPage * 64 * (int)sizeof(TKV));
   const int s_cap = nwg / hkv;
-  const int nsplit_min = (npg + kv_cap - 1) / kv_cap;
-  const bool per_q = hq * nsplit_min <= nwg;
-  const int nh = per_q ? 1 : G;                 // query heads per item
-  int nspl = per_q ? nsplit_min : (nsplit_min < s_cap ? nsplit_min : s_cap);
-  const int pps = (npg + nspl - 1) / nspl;      // pages per split
-  nspl = (npg + pps - 1) / pps;
-  const int n_items = (hq / nh) * nspl;
-  const bool has_item = wg < n_items;
-  const int it_h = wg / nspl, it_sp = wg % nspl;          // head set, split
-  const int it_g = per_q ? it_h / G : it_h;               // kv head
-  const int it_j0 = per_q ? it_h : it_h * G;              // first query head
-  const int ngrp = kStepWaves / nh;                       // waves per query head
-  const int it_pg0 = it_sp * pps, it_pg1 = min(npg, it_pg0 + pps);
 
-  // Phase table: sequence index i -> (layer, kind) with four GEMV phases per
-  // layer and the LM head last.
-  auto phase_w = [&](int l, int kind) -> const TW* {
-    if (kind == PH_HEAD) return P.head;
-    const LayerPtrs<TW>& Lw = lptr[l];
-    return kind == PH_QKV ? Lw.wqkv : kind == PH_O ? Lw.wo : kind == PH_GU ? Lw.wgu : Lw.wdown;
-  };
-  auto phase_k = [&](int kind) { return kind == PH_DOWN ? F : kind == PH_O ? hq * 64 : d; };
-  auto phase_map = [&](int kind) -> RowMap {
-    if (kind == PH_QKV) return RowMap{1, pq0, 0, F};
-    if (kind == PH_GU) return RowMap{2, j0, j1 - j0, F};
-    return RowMap{0, kind == PH_HEAD ? v0 : rd0, 0, F};
-  };
-  auto phase_n = [&](int kind) {
-    return kind == PH_QKV ? 2 * (pq1 - pq0) : kind == PH_GU ? 2 * (j1 - j0) : kind == PH_HEAD ? v1 - v0 : nd;
-  };
+  char* ring = smem;
+  float* xa = reinterpret_cast<float*>(smem + (size_t)S * kSlot);  // [d] normalised inputs (QKV, GU, head)
+  float* xc = xa + d;                                               // [F] or [Hq*64] + attention states
+  float* res = xc + step_xc_floats(d, hq, hkv);  // [kStepResFloats] phase results
+  float* xown = res + kStepResFloats;                               // [kStepResFloats] this workgroup's rows of x
+  float* st = xc + hq * 64;                                         // [kNC][G][kStRow] attention states
 
-  WBuf wb;              // the next phase's first weight batch, in flight
-  float gr[kNormRegs];  // the next phase's RMSNorm gains, elements tid + 512 k
-  auto issue_first = [&](int l2, int k2) {
-    // Gains first: the norm needs them as soon as the input arrives, and a
-    // wave's loads complete in order.
-    const float* gsrc = k2 == PH_QKV ? lptr[l2].attn_norm
-                        : k2 == PH_GU ? lptr[l2].mlp_norm
-                        : k2 == PH_HEAD ? P.final_norm : nullptr;
-    if (gsrc) {
-#pragma unroll
-      for (int k = 0; k < kNormRegs; ++k) {
-        const int i = tid + k * kStepThreads;
-        gr[k] = i < d ? gsrc[i] : 0.f;
-      }
-    }
-    if (k2 == PH_DOWN) RowBatch<TW, CHF>::issue(wb, phase_w(l2, k2), F, phase_map(k2), phase_n(k2), 0);
-    else RowBatch<TW, CHD>::issue(wb, phase_w(l2, k2), phase_k(k2), phase_map(k2), phase_n(k2), 0);
-  };
-  // Everything the epilogues read from memory is loaded now, so no epilogue
-  // load ever queues behind a phase's weight or KV stream.
-  const int page_p = P.page_table[(size_t)s * P.kv.max_pages + p / kPage];  // page of this position
+  Plan pl;
+  make_plan<TW, TKV, NPD>(pl, P, wg, nwg, t);
+  const int nd = pl.rd1 - pl.rd0;
+
+  if (tid < kMaxRing) {
+    syp->consumed[tid] = tid - S;
+    syp->landed[tid] = tid - S;
+  }
+  if (tid == 0) {
+    syp->quiet = 0;
+    syp->cbar = 0;
+    syp->abort = 0;
+  }
   if (tid < 32) rope_p[tid] = P.rope[(size_t)p * 32 + tid];
   for (int i = tid; i < L; i += kStepThreads) lptr[i] = P.layer[i];
-  if (has_item)
-    for (int i = tid; i < it_pg1 - it_pg0; i += kStepThreads)
-      item_pages[i] = P.page_table[(size_t)s * P.kv.max_pages + it_pg0 + i];
+  if (pl.has_item)
+    for (int i = tid; i < pl.it_pg1 - pl.it_pg0; i += kStepThreads)
+      item_pages[i] = P.page_table[(size_t)s * P.kv.max_pages + pl.it_pg0 + i];
   const TW* erow = P.embed + (size_t)tok * d;
-  for (int i = tid; i < nd; i += kStepThreads) xown[i] = (float)erow[rd0 + i];
+  for (int i = tid; i < nd; i += kStepThreads) xown[i] = (float)erow[pl.rd0 + i];
+  const int page_p = P.page_table[(size_t)s * P.kv.max_pages + p / kPage];  // page receiving this position
   __syncthreads();
-  issue_first(0, L > 0 ? PH_QKV : PH_HEAD);
 
-  // Issue direct global->LDS loads of pages [pa, pb) of kv head it_g, layer
-  // l: wave instruction q moves 1 KiB (lane i: 16 bytes at offset 16 i).
-  auto stage_kv = [&](int l, int pa, int pb) {
-    constexpr int tile_kib = kPage * 64 * (int)sizeof(TKV) / 1024;  // 1 KiB pieces per K or V tile
-    const int n_instr = (pb - pa) * 2 * tile_kib;
-    for (int q = wave; q < n_instr; q += kStepWaves) {
-      const int tile = q / tile_kib, piece = q % tile_kib;
-      const int pl = tile >> 1, kind2 = tile & 1;
-      const int page = item_pages[pa + pl - it_pg0];
-      const char* src = reinterpret_cast<const char*>(P.kvc + P.kv.head_tile(l, page, kind2, it_g)) +
-                        piece * 1024 + lane * 16;
-      char* dst = reinterpret_cast<char*>(kvs + (size_t)tile * kPage * 64) + piece * 1024;
-      __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+  // ================================================================ streaming waves
+  // Wave lw streams the slots n with n % kLoaders == lw.  After issuing one,
+  // it waits until at most `depth` of its slots are in flight and marks the
+  // oldest as landed.
+  if (wave < kLoaders) {
+    __builtin_amdgcn_s_setprio(3);  // issue ahead of the compute wave sharing this SIMD
+    const int lw = wave;
+    const int depth = P.load_depth < 1 ? 1 : P.load_depth > 7 ? 7 : P.load_depth;
+    int n = 0;                      // slot index in the stream
+    int mypub = lw - kLoaders;      // this wave's last slot marked landed
+    unsigned long long stall = 0;
+    auto publish_upto = [&](int upto) {  // mark this wave's slots <= upto landed
+      while (mypub + kLoaders <= upto) {
+        mypub += kLoaders;
+        if (lane == 0) *(volatile int HH_LDS*)&syp->landed[mypub % S] = mypub;
+      }
+    };
+    // Per-lane byte offsets of the two 1 KiB halves of a swizzled fp16 K/V
+    // tile: lane i fills LDS chunk i, i.e. key 8 h + i / 8, chunk position
+    // i % 8, which holds the key's source chunk (i % 8) ^ ((key / 2) % 8).
+    int kvoff[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int key = 8 * h + (lane >> 3);
+      kvoff[h] = key * 128 + (((lane & 7) ^ ((key >> 1) & 7)) << 4);
+    }
+    for (int l = 0; l <= L; ++l) {
+      if (lw == 0 && P.trace && lane == 0) P.trace[((size_t)wg * (L + 1) + l) * 32 + 20] = wall_clock64();
+      stall = 0;
+      for (int sg = (l < L ? SG_QKV : SG_HEAD); sg <= (l < L ? SG_DOWN : SG_HEAD); ++sg) {
+        const int nsl = pl.slots(sg);
+        if (nsl == 0) continue;
+        // The segment's matrix, rows and row size.
+        const char* W = nullptr;
+        RowMap map{0, 0, 0, F};
+        int nrows = 0, rowb = 0;
+        if (sg != SG_KV) {
+          rowb = d * (int)sizeof(TW);
+          if (sg == SG_QKV) {
+            W = reinterpret_cast<const char*>(lptr[l].wqkv);
+            map = RowMap{1, pl.pq0, 0, F};
+            nrows = 2 * (pl.pq1 - pl.pq0);
+          } else if (sg == SG_O) {
+            W = reinterpret_cast<const char*>(lptr[l].wo);
+            map = RowMap{0, pl.rd0, 0, F};
+            nrows = nd;
+          } else if (sg == SG_GU) {
+            W = reinterpret_cast<const char*>(lptr[l].wgu);
+            map = RowMap{2, pl.j0, pl.j1 - pl.j0, F};
+            nrows = 2 * (pl.j1 - pl.j0);
+          } else if (sg == SG_DOWN) {
+            W = reinterpret_cast<const char*>(lptr[l].wdownT);
+            map = RowMap{0, pl.j0, 0, F};
+            nrows = pl.j1 - pl.j0;
+          } else {
+            W = reinterpret_cast<const char*>(P.head);
+            map = RowMap{0, pl.v0, 0, F};
+            nrows = pl.v1 - pl.v0;
+          }
+        }
+        const bool full = (rowb & 1023) == 0;
+        const int base = n;  // stream index of the segment's first slot
+        for (int k = (lw - base % kLoaders + kLoaders) % kLoaders; k < nsl; k += kLoaders) {
+          const int m = base + k, pos = m % S;
+          // Wait for a free ring position; first mark everything in flight
+          // landed, so compute waves never wait on slots held back here.
+          if (*(volatile int HH_LDS*)&syp->consumed[pos] < m - S) {
+            const unsigned long long t0s = wall_clock64();
+            if (lw == 0 && P.trace && lane == 0 && stall == 0) P.trace[((size_t)wg * (L + 1) + l) * 32 + 23] = t0s;
+            HH_STEP_VMWAIT(0);
+            compiler_fence();
+            publish_upto(m - kLoaders);
+            unsigned spins = 0;
+            unsigned long long t0 = 0;
+            while (*(volatile int HH_LDS*)&syp->consumed[pos] < m - S) {
+              __builtin_amdgcn_s_sleep(1);
+              if (give_up(spins, t0, syp, (int HH_GLB*)P.err)) break;
+            }
+            compiler_fence();
+            stall += wall_clock64() - t0s;
+          }
+          // Optionally keep HBM quiet while this workgroup's compute waves wait
+          // for other workgroups (shorter exchange latency, less prefetch).
+          // quiet 1: stop issuing; quiet 2: keep at most one slot in flight.
+          if (P.quiet == 1 && *(volatile int HH_LDS*)&syp->quiet) {
+            HH_STEP_VMWAIT(0);
+            compiler_fence();
+            publish_upto(m - kLoaders);
+            unsigned spins = 0;
+            unsigned long long t0 = 0;
+            while (*(volatile int HH_LDS*)&syp->quiet) {
+              __builtin_amdgcn_s_sleep(1);
+              if (give_up(spins, t0, syp, (int HH_GLB*)P.err)) break;
+            }
+            compiler_fence();
+          } else if (P.quiet == 2 && *(volatile int HH_LDS*)&syp->quiet) {
+            HH_STEP_VMWAIT(0);
+            compiler_fence();
+            publish_upto(m - kLoaders);
+          }
+          char* dst = ring + (size_t)pos * kSlot;
+          if (sg == SG_KV) {
+            // K/V pages of the item: fp16 tiles swizzled (2 pages per slot:
+            // [K a][V a][K b][V b]), fp32 tiles plain (1 page: [K][V]).
+            const int pg_a = pl.it_pg0 + k * pl.pps;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              const char* src;
+              if constexpr (sizeof(TKV) == 2) {
+                const int pg = pg_a + (q >> 2);
+                const int pgv = pg < pl.it_pg1 ? pg : pg_a;  // a missing page b repeats page a
+                const int phys = item_pages[pgv - pl.it_pg0];
+                const int kind = (q >> 1) & 1;
+                src = reinterpret_cast<const char*>(P.kvc + P.kv.head_tile(l, phys, kind, pl.it_g)) + kvoff[q & 1];
+              } else {
+                const int phys = item_pages[pg_a - pl.it_pg0];
+                const int kind = q >> 2;
+                const int key = (q & 3) * 4 + (lane >> 4);
+                src = reinterpret_cast<const char*>(P.kvc + P.kv.head_tile(l, phys, kind, pl.it_g)) + key * 256 +
+                      (lane & 15) * 16;
+              }
+              __builtin_amdgcn_global_load_lds(src, dst + q * 1024, 16, 0, 0);
+            }
+          } else {
+            issue_row_slot<NPD>(dst, W, map, rowb, nrows, k, full);
+          }
+          // Keep at most `depth` of this wave's slots in flight.
+          switch (depth) {
+            case 1: HH_STEP_VMWAIT(0); break;
+            case 2: HH_STEP_VMWAIT(8); break;
+            case 3: HH_STEP_VMWAIT(16); break;
+            case 4: HH_STEP_VMWAIT(24); break;
+            case 5: HH_STEP_VMWAIT(32); break;
+            case 6: HH_STEP_VMWAIT(40); break;
+            default: HH_STEP_VMWAIT(48); break;
+          }
+          compiler_fence();
+          publish_upto(m - kLoaders * (depth - 1));
+        }
+        n = base + nsl;
+      }
+      if (lw == 0 && P.trace && lane == 0) {
+        P.trace[((size_t)wg * (L + 1) + l) * 32 + 21] = stall;
+        P.trace[((size_t)wg * (L + 1) + l) * 32 + 22] = wall_clock64();
+      }
+    }
+    HH_STEP_VMWAIT(0);
+    compiler_fence();
+    publish_upto(n - 1);
+    return;
+  }
+
+  // ================================================================ compute waves
+  const int cw = wave - kLoaders;
+  int gen = 0;  // compute-wave barrier generation
+  int HH_GLB* err = (int HH_GLB*)P.err;
+
+  // Stage x (words at epoch ep, or the embedding row when src is null) times
+  // the RMSNorm gain into xa; returns 1 / rms after a compute-wave barrier.
+  auto quiet = [&](int on) {
+    if (cw == 0 && lane == 0) *(volatile int HH_LDS*)&syp->quiet = on;
+  };
+  auto tr = [&](int l, int ev) {
+    return PollTrace{P.trace ? P.trace + ((size_t)wg * (L + 1) + l) * 32 + ev : nullptr};
+  };
+  auto stage_norm = [&](const unsigned long long* src, unsigned ep, const float* gain, PollTrace pt) -> float {
+    quiet(1);
+    float ss = 0.f;
+    const int tc = tid - 64 * kLoaders;
+    if (src) {
+      // The gains are loaded before the words are polled, so they never
+      // cost a round trip of their own after the words arrive.
+      for (int base = tc; base < d; base += kNC * 64 * kPollX) {
+        float gr[kPollX];
+#pragma unroll
+        for (int u = 0; u < kPollX; ++u) {
+          const int i = base + u * kNC * 64;
+          gr[u] = i < d ? ((const float HH_GLB*)gain)[i] : 0.f;
+        }
+        poll_words<kPollX>([=](int i) { return src + base - tc + i; }, d - (base - tc), ep, syp, err,
+                           [&](int i, float v) {
+                             const int u = (i - tc) / (kNC * 64);
+                             float g = 0.f;
+#pragma unroll
+                             for (int q = 0; q < kPollX; ++q) g = q == u ? gr[q] : g;
+                             xa[base - tc + i] = v * g;
+                             ss = fmaf(v, v, ss);
+                           },
+                           pt);
+      }
+    } else {
+      for (int i = tc; i < d; i += kNC * 64) {
+        const float v = (float)erow[i];
+        xa[i] = v * ((const float HH_GLB*)gain)[i];
+        ss = fmaf(v, v, ss);
+      }
+    }
+    ss = wave_sum_u(ss);
+    if (lane == 0) syp->ss[cw] = ss;
+    cbar(syp, gen, err);
+    quiet(0);
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kNC; ++w) tot += syp->ss[w];
+    return rsqrtf(tot / (float)d + P.eps);
+  };
+
+  // Consume this wave's slots of a row segment (global slot index base);
+  auto run_rows = [&](int base, int nsl, const float* xs, int K, int nrows) {
+    for (int k = cw; k < nsl; k += kNC) {
+      const int n = base + k, pos = n % S;
+      wait_landed(syp, n, pos, err);
+      slot_rows<TW, NPD, FD>(ring + (size_t)pos * kSlot, xs, K, k, nrows, res);
+      release_slot(syp, pos, n);
     }
   };
 
-  const int nphase = 4 * L + 1;
-  for (int ip = 0; ip < nphase; ++ip) {
-    const int l = ip == 4 * L ? L : ip >> 2;
-    const int kind = ip == 4 * L ? PH_HEAD : ip & 3;
+  float inv = 1.f;
+  for (int l = 0; l < L; ++l) {
+    const int lbase = l * pl.per_layer;
 
-    // ---- paged GQA attention, before the O projection (workgroups with an
-    // item; a wave's loads complete in order, so these workgroups issue their
-    // O-projection prefetch only after it).
-    if (kind == PH_O && has_item) {
-      const int g = it_g, sp = it_sp;
-      const unsigned e0 = ep_of(E0, l, 0);
-      const int jj = wave % nh, grp = wave / nh;
-      const int key = lane >> 2, quarter = lane & 3;
-      // The item's query heads and the current position's k, v.
-      for (int i = tid; i < nh * 64 + 128; i += kStepThreads) {
-        const unsigned long long* src = i < nh * 64 ? P.ll_q + it_j0 * 64 + i
-                                        : i < nh * 64 + 64 ? P.ll_kn + g * 64 + (i - nh * 64)
-                                                           : P.ll_vn + g * 64 + (i - nh * 64 - 64);
-        const float v = __uint_as_float(ll_wait(src, e0, ll_get(src), P.err));
-        if (i < nh * 64) qs[i] = v;
-        else if (i < nh * 64 + 64) kn[i - nh * 64] = v;
-        else vn[i - nh * 64 - 64] = v;
-      }
-      STEP_MARK(l, 12);
-      const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
-      float m = -INFINITY, lsum = 0.f, o[16], qv[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[e] = 0.f;
-      for (int ca = it_pg0; ca < it_pg1; ca += kv_cap) {
-        const int cb = min(it_pg1, ca + kv_cap);
-        if (ca != it_pg0) stage_kv(l, ca, cb);
-        __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads have landed
-        __syncthreads();
-        if (ca == it_pg0) STEP_MARK(l, 16);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) qv[e] = qs[jj * 64 + quarter * 16 + e] * qscale;
-        for (int pg = ca + grp; pg < cb; pg += ngrp) {
-          const TKV* Kl = kvs + (size_t)((pg - ca) * 2) * kPage * 64 + key * 64 + quarter * 16;
-          const TKV* Vl = Kl + kPage * 64;
-          float kf[16], vf[16];
-#pragma unroll
-          for (int e = 0; e < 16; e += Vec16<TKV>::n) {
-            widen16(*reinterpret_cast<const u32x4*>(Kl + e), kf + e, TKV());
-            widen16(*reinterpret_cast<const u32x4*>(Vl + e), vf + e, TKV());
-          }
-          if (pg * kPage + key == p) {  // written this step: take the exchanged copy
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              kf[e] = kn[quarter * 16 + e];
-              vf[e] = vn[quarter * 16 + e];
-            }
-          }
-          float sc = 0.f;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) sc = fmaf(qv[e], kf[e], sc);
-          sc += dpp<0xB1>(sc);  // the 4 lanes of a key hold quarters of its dot product
-          sc += dpp<0x4E>(sc);
-          if (pg * kPage + key >= t) {  // a slot past the length: stale data, weight 0 (and 0 * NaN is NaN)
-            sc = -INFINITY;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) vf[e] = 0.f;
-          }
-          const float mn = fmaxf(m, wave_max_u(sc));
-          const float alpha = exp2f(m - mn);
-          const float pk = exp2f(sc - mn);
-          lsum = lsum * alpha + (quarter == 0 ? pk : 0.f);
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[e] = fmaf(pk, vf[e], o[e] * alpha);
-          m = mn;
-        }
-        __syncthreads();  // the stage is reused by the next chunk
-      }
-      // Reduce over the keys of each row (lanes of a row sharing `quarter`;
-      // row_ror by 4 and 8 keeps lane bits 0-1), then across the 4 rows in
-      // the merge below: lanes 0-3 of row r leave o[quarter*16 .. +16] in
-      // the wave's state slot for row r.
-      lsum = wave_sum_u(lsum);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float v = o[e];
-        v += dpp<0x124>(v);
-        v += dpp<0x128>(v);
-        o[e] = v;
-      }
-      {
-        float* sw = st + wave * 4 * 66 + (lane >> 4) * 66;
-        if ((lane & 15) == 0) {
-          sw[0] = m;
-          sw[1] = lsum;
-        }
-        if ((lane & 15) < 4) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) sw[2 + quarter * 16 + e] = o[e];
-        }
-      }
-      __syncthreads();
-      // Merge the wave groups of each query head (one wave per head).
-      if (wave < nh) {
-        const int j = it_j0 + wave;
-        float M = -INFINITY;
-        for (int gr = 0; gr < ngrp; ++gr) M = fmaxf(M, st[(gr * nh + wave) * 4 * 66]);
-        float Ls = 0.f, O = 0.f;
-        for (int gr = 0; gr < ngrp; ++gr) {
-          const float* sw = st + (gr * nh + wave) * 4 * 66;
-          const float f = exp2f(sw[0] - M);
-          Ls = fmaf(sw[1], f, Ls);
-          const float ow = (sw[2 + lane] + sw[66 + 2 + lane]) + (sw[132 + 2 + lane] + sw[198 + 2 + lane]);
-          O = fmaf(ow, f, O);
-        }
-        if (nspl == 1) {
-          ll_put(P.ll_o + j * 64 + lane, O / Ls, ep_of(E0, l, 2));
-        } else {
-          unsigned long long* pp = P.ll_part + ((size_t)j * s_cap + sp) * 66;
-          const unsigned e1 = ep_of(E0, l, 1);
-          if (lane == 0) {
-            ll_put(pp, M, e1);
-            ll_put(pp + 1, Ls, e1);
-          }
-          ll_put(pp + 2 + lane, O, e1);
-        }
-      }
-      __syncthreads();
-      STEP_MARK(l, 13);
-      // Split 0 combines the splits of its query heads: wave (head jj, group
-      // grp) loads splits grp, grp + ngrp, ... a round of 8 at a time (lane =
-      // head dimension), then the groups merge through LDS.
-      if (nspl > 1 && sp == 0) {
-        const unsigned e1 = ep_of(E0, l, 1);
-        float M = -INFINITY, Ls = 0.f, O = 0.f;
-        {
-          const int j = it_j0 + jj;
-          const unsigned long long* pp = P.ll_part + (size_t)j * s_cap * 66;
-          for (int r0 = grp; r0 < nspl; r0 += kMaxSplitsPerWave * ngrp) {
-            unsigned long long w[kMaxSplitsPerWave][3];
-            unsigned stale = 0;
-#pragma unroll
-            for (int u = 0; u < kMaxSplitsPerWave; ++u) {
-              const int i = r0 + u * ngrp;
-              const unsigned long long* q0 = pp + (size_t)i * 66;
-              w[u][0] = w[u][1] = w[u][2] = (unsigned long long)e1 << 32;
-              if (i < nspl) {
-                w[u][0] = ll_get(q0);
-                w[u][1] = ll_get(q0 + 1);
-                w[u][2] = ll_get(q0 + 2 + lane);
-              }
-            }
-#pragma unroll
-            for (int u = 0; u < kMaxSplitsPerWave; ++u)
-              stale |= ((unsigned)(w[u][0] >> 32) != e1 || (unsigned)(w[u][1] >> 32) != e1 ||
-                                (unsigned)(w[u][2] >> 32) != e1
-                            ? 1u
-                            : 0u)
-                       << u;
-            unsigned spins = 0;
-            while (stale) {
-              __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-              for (int u = 0; u < kMaxSplitsPerWave; ++u)
-                if (stale & (1u << u)) {
-                  const unsigned long long* q0 = pp + (size_t)(r0 + u * ngrp) * 66;
-                  w[u][0] = ll_get(q0);
-                  w[u][1] = ll_get(q0 + 1);
-                  w[u][2] = ll_get(q0 + 2 + lane);
-                  if ((unsigned)(w[u][0] >> 32) == e1 && (unsigned)(w[u][1] >> 32) == e1 &&
-                      (unsigned)(w[u][2] >> 32) == e1)
-                    stale &= ~(1u << u);
-                }
-              if ((++spins & 255u) == 0 && stale) {
-                if (spins > kSpinLimit || __hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                  __hip_atomic_store(P.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                  break;
-                }
-              }
-            }
-#pragma unroll
-            for (int u = 0; u < kMaxSplitsPerWave; ++u) {
-              if (r0 + u * ngrp >= nspl) break;
-              const float mi = __uint_as_float((unsigned)w[u][0]);
-              const float li = __uint_as_float((unsigned)w[u][1]);
-              const float oi = __uint_as_float((unsigned)w[u][2]);
-              const float Mn = fmaxf(M, mi);
-              const float a = exp2f(M - Mn), b = exp2f(mi - Mn);
-              Ls = Ls * a + li * b;
-              O = O * a + oi * b;
-              M = Mn;
-            }
-          }
-        }
-        float* sw = st + wave * 4 * 66;
-        if (lane == 0) {
-          sw[0] = M;
-          sw[1] = Ls;
-        }
-        sw[2 + lane] = O;
-        __syncthreads();
-        if (wave < nh) {
-          float Mx = -INFINITY;
-          for (int gr = 0; gr < ngrp; ++gr) Mx = fmaxf(Mx, st[(gr * nh + wave) * 4 * 66]);
-          float Lt = 0.f, Ot = 0.f;
-          for (int gr = 0; gr < ngrp; ++gr) {
-            const float* sv = st + (gr * nh + wave) * 4 * 66;
-            const float f = exp2f(sv[0] - Mx);
-            Lt = fmaf(sv[1], f, Lt);
-            Ot = fmaf(sv[2 + lane], f, Ot);
-          }
-          ll_put(P.ll_o + (it_j0 + wave) * 64 + lane, Ot / Lt, ep_of(E0, l, 2));
-        }
-        __syncthreads();
-        STEP_MARK(l, 14);
-      }
-      issue_first(l, PH_O);
-    }
-
-    // ---- stage this phase's input vector into LDS (normalised where needed)
-    STEP_MARK(l, kind * 3);
-    {
-      const bool normed = kind == PH_QKV || kind == PH_GU || kind == PH_HEAD;
-      float ss;
-      if ((kind == PH_QKV && l == 0) || (kind == PH_HEAD && L == 0)) {  // the embedding row itself
-        ss = 0.f;
-        for (int i = tid; i < d; i += kStepThreads) {
-          const float v = (float)erow[i];
-          xs[i] = v;
-          ss += v * v;
-        }
-        ss = wave_sum(ss);
-        if (lane == 0) red[wave] = ss;
-        __syncthreads();
-        ss = 0.f;
-        for (int w = 0; w < kStepWaves; ++w) ss += red[w];
-        __syncthreads();
-      } else {
-        const unsigned long long* src = kind == PH_QKV || kind == PH_HEAD ? P.ll_xb
-                                        : kind == PH_O ? P.ll_o : kind == PH_GU ? P.ll_xa : P.ll_m;
-        const int n = kind == PH_O ? hq * 64 : kind == PH_DOWN ? F : d;
-        const unsigned e = kind == PH_QKV || kind == PH_HEAD ? ep_of(E0, l - 1, 5)
-                           : ep_of(E0, l, kind == PH_O ? 2 : kind == PH_GU ? 3 : 4);
-        ss = ll_stage(src, n, e, xs, red, P.err);
-      }
-      if (normed) norm_staged<kNormRegs>(xs, d, ss, P.eps, gr);
-    }
-    STEP_MARK(l, kind * 3 + 1);
-
-    // ---- stream this workgroup's weight rows
-    const int nl = phase_n(kind);
-    if (kind == PH_DOWN) run_rows<TW, CHF>(wb, phase_w(l, kind), F, phase_map(kind), nl, xs, res);
-    else run_rows<TW, CHD>(wb, phase_w(l, kind), phase_k(kind), phase_map(kind), nl, xs, res);
-    __syncthreads();
-    STEP_MARK(l, kind * 3 + 2);
-    // Cached pages do not depend on this step: start staging this layer's
-    // attention K/V now, so it streams during the epilogue and the q wait.
-    if (kind == PH_QKV && has_item) stage_kv(l, it_pg0, min(it_pg1, it_pg0 + kv_cap));
-
-    // ---- epilogue
-    if (kind == PH_QKV) {
+    // ---------------------------------------------------- RMSNorm + QKV + RoPE
+    STEP_MARK(l, 0);
+    inv = stage_norm(l == 0 ? nullptr : P.ll_xb, ep_of(E0, l - 1, 5), lptr[l].attn_norm, tr(l, 24));
+    STEP_MARK(l, 1);
+    run_rows(lbase + pl.o_qkv, pl.n_qkv, xa, d, 2 * (pl.pq1 - pl.pq0));
+    cbar(syp, gen, err);
+    STEP_MARK(l, 2);
+    if (cw == 0) {
       const unsigned e = ep_of(E0, l, 0);
-      for (int lp = tid; lp < (pq1 - pq0); lp += kStepThreads) {
-        const int gp = pq0 + lp, head = gp >> 5, i = gp & 31;
-        const float y0 = res[2 * lp], y1 = res[2 * lp + 1];
+      for (int lp = lane; lp < pl.pq1 - pl.pq0; lp += 64) {
+        const int gp = pl.pq0 + lp, head = gp >> 5, i = gp & 31;
+        const float y0 = res[2 * lp] * inv, y1 = res[2 * lp + 1] * inv;
         if (head < hq + hkv) {
           const float2 cs = rope_p[i];
           const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
@@ -711,86 +793,590 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
           ll_put(P.ll_vn + g * 64 + i + 32, (float)(TKV)y1, e);
         }
       }
-    } else if (kind == PH_O || kind == PH_DOWN) {
-      unsigned long long* dst = kind == PH_O ? P.ll_xa : P.ll_xb;
-      const unsigned e = ep_of(E0, l, kind == PH_O ? 3 : 5);
-      for (int i = tid; i < nd; i += kStepThreads) {
+    }
+    STEP_MARK(l, 3);
+
+    // ---------------------------------------------------- attention item
+    if (pl.has_item) {
+      STEP_MARK(l, 4);
+      const int g = pl.it_g, j0 = g * G;
+      const unsigned e0 = ep_of(E0, l, 0);
+      const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
+      {
+        // One poll over the item's query heads, then the key and value of
+        // the current position (offsets from ll_q: a select among three
+        // pointers would be lowered to a table in scratch memory).
+        const unsigned long long* qb = P.ll_q;
+        const int oq = j0 * 64, ok = (int)(P.ll_kn - P.ll_q) + g * 64 - G * 64,
+                  ov = (int)(P.ll_vn - P.ll_q) + g * 64 - G * 64 - 64;
+        quiet(1);
+        poll_words<2>(
+            [=](int i) { return qb + i + oq + (i >= G * 64 ? ok - oq : 0) + (i >= G * 64 + 64 ? ov - ok : 0); }, G * 64 + 128, e0,
+            syp, err, [&](int i, float v) {
+              if (i < G * 64) qs[i] = v * qscale;
+              else if (i < G * 64 + 64) kn[i - G * 64] = v;
+              else vn[i - G * 64 - 64] = v;
+            });
+      }
+      cbar(syp, gen, err);
+      quiet(0);
+      STEP_MARK(l, 5);
+      const int kbase = lbase + pl.o_kv;
+      const int nsl = pl.n_kv;
+      const int key_base = pl.it_pg0 * kPage;
+      const int kend = t < pl.it_pg1 * kPage ? t : pl.it_pg1 * kPage;  // keys of this item: [key_base, kend)
+      float* stw = st + (size_t)cw * G * kStRow;
+      if constexpr (sizeof(TKV) == 2) {
+        // ---- fp16 K/V: 16x16x32 MFMAs.  S^T[key][head] = K Q^T, lane l:
+        // head l % 16, keys 4 (l / 16) + r of each 16-key tile; then
+        // O^T[dim][head] += V^T P^T with the contraction's key order chosen
+        // so P goes from the score accumulators straight into the B operand.
+        const int hcol = lane & 15, grp = lane >> 4;
+        f16x8v qh[2], ql[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float v = hcol < G ? qs[hcol * 64 + 32 * hh + 8 * grp + e] : 0.f;
+            const _Float16 hi = (_Float16)v;
+            qh[hh][e] = hi;
+            ql[hh][e] = (_Float16)(v - (float)hi);
+          }
+        float m = -INFINITY, lsum = 0.f;
+        f32x4 oacc[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) oacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int k = cw; k < nsl; k += kNC) {
+          const int n = kbase + k, pos = n % S;
+          const int key0 = key_base + k * 32;  // position of the slot's first key
+          wait_landed(syp, n, pos, err);
+          char* slot = ring + (size_t)pos * kSlot;
+          // The slot holding this step's position gets the exchanged key and
+          // value (its cache row may not have been written yet when it was
+          // streamed); rows past the item's last key get zero values (stale
+          // or foreign slots: weight 0, and 0 * NaN would be NaN).
+          if (key0 + 32 > kend) {
+            if (p >= key0 && p < kend) {
+              const int kk = p - key0, tt = kk >> 4, key = kk & 15;
+              const int off = tt * 4096 + key * 128 + ((((lane >> 3) ^ ((key >> 1) & 7))) << 4) + (lane & 7) * 2;
+              *reinterpret_cast<_Float16*>(slot + off) = (_Float16)kn[lane];
+              *reinterpret_cast<_Float16*>(slot + off + 2048) = (_Float16)vn[lane];
+            }
+            for (int r = kend - key0 + (lane >> 3); r < 32; r += 8)
+              *reinterpret_cast<u32x4*>(slot + (r >> 4) * 4096 + 2048 + (r & 15) * 128 + (lane & 7) * 16) =
+                  u32x4{0u, 0u, 0u, 0u};
+          }
+          f32x4 sc[2];
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt) {
+            sc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int key = lane & 15;
+            const char* Kt = slot + tt * 4096;
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int c = 4 * hh + grp;
+              const f16x8v a = *reinterpret_cast<const f16x8v*>(Kt + key * 128 + ((c ^ ((key >> 1) & 7)) << 4));
+              sc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, qh[hh], sc[tt], 0, 0, 0);
+              sc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, ql[hh], sc[tt], 0, 0, 0);
+            }
+          }
+          float bm = -INFINITY;
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int kp = key0 + 16 * tt + 4 * grp + r;
+              const float v = kp < kend ? sc[tt][r] : -INFINITY;
+              sc[tt][r] = v;
+              bm = fmaxf(bm, v);
+            }
+          bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+          bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+          const float mn = fmaxf(m, bm);  // finite: the slot's first key is in the item
+          const float alpha = exp2f(m - mn);
+          f16x8v pb;
+          float ls = 0.f;
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float pv = exp2f(sc[tt][r] - mn);
+              ls += pv;
+              pb[4 * tt + r] = (_Float16)pv;
+            }
+          lsum = lsum * alpha + ls;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt) {
+            const int dim = 16 * dt + hcol;
+            f16x8v a;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int tt = e >> 2, kk = 4 * grp + (e & 3);
+              a[e] = *reinterpret_cast<const _Float16*>(slot + tt * 4096 + 2048 + kk * 128 +
+                                                        ((((dim >> 3) ^ ((kk >> 1) & 7))) << 4) + (dim & 7) * 2);
+            }
+            oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, pb, oacc[dt], 0, 0, 0);
+          }
+          m = mn;
+          release_slot(syp, pos, n);
+        }
+        lsum += __shfl_xor(lsum, 16, 64);
+        lsum += __shfl_xor(lsum, 32, 64);
+        if (hcol < G) {
+          float* sh = stw + hcol * kStRow;
+          if (grp == 0) {
+            sh[0] = m;
+            sh[1] = lsum;
+          }
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sh[2 + 16 * dt + 4 * grp + r] = oacc[dt][r];
+        }
+      } else {
+        // ---- fp32 K/V (one page per slot): VALU.  Lane l: key l / 4,
+        // dims 16 (l % 4) .. + 16; G query heads at once.
+        const int key = lane >> 2, quarter = lane & 3;
+        float m[kMaxGroupF32], lsum[kMaxGroupF32], o[kMaxGroupF32][16];
+#pragma unroll
+        for (int h = 0; h < kMaxGroupF32; ++h) {
+          m[h] = -INFINITY;
+          lsum[h] = 0.f;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[h][e] = 0.f;
+        }
+        for (int k = cw; k < nsl; k += kNC) {
+          const int n = kbase + k, pos = n % S;
+          const int kp = key_base + k * kPage + key;
+          wait_landed(syp, n, pos, err);
+          const float* Kt = reinterpret_cast<const float*>(ring + (size_t)pos * kSlot) + key * 64 + quarter * 16;
+          const float* Vt = Kt + kPage * 64;
+          float kf[16], vf[16];
+#pragma unroll
+          for (int e = 0; e < 16; e += 4) {
+            const float4 a = *reinterpret_cast<const float4*>(Kt + e);
+            const float4 b = *reinterpret_cast<const float4*>(Vt + e);
+            kf[e] = a.x; kf[e + 1] = a.y; kf[e + 2] = a.z; kf[e + 3] = a.w;
+            vf[e] = b.x; vf[e + 1] = b.y; vf[e + 2] = b.z; vf[e + 3] = b.w;
+          }
+          if (kp == p) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              kf[e] = kn[quarter * 16 + e];
+              vf[e] = vn[quarter * 16 + e];
+            }
+          }
+          if (kp >= kend) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) vf[e] = 0.f;
+          }
+          release_slot(syp, pos, n);
+#pragma unroll
+          for (int h = 0; h < kMaxGroupF32; ++h) {
+            if (h < G) {
+              float sc = 0.f;
+#pragma unroll
+              for (int e = 0; e < 16; ++e) sc = fmaf(qs[h * 64 + quarter * 16 + e], kf[e], sc);
+              sc += dpp<0xB1>(sc);
+              sc += dpp<0x4E>(sc);
+              if (kp >= kend) sc = -INFINITY;
+              const float mn = fmaxf(m[h], wave_max_u(sc));
+              const float alpha = exp2f(m[h] - mn);
+              const float pk = exp2f(sc - mn);
+              lsum[h] = lsum[h] * alpha + (quarter == 0 ? pk : 0.f);
+#pragma unroll
+              for (int e = 0; e < 16; ++e) o[h][e] = fmaf(pk, vf[e], o[h][e] * alpha);
+              m[h] = mn;
+            }
+          }
+        }
+#pragma unroll
+        for (int h = 0; h < kMaxGroupF32; ++h) {
+          if (h < G) {
+            const float lt = wave_sum_u(lsum[h]);
+            float* sh = stw + h * kStRow;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              float v = o[h][e];
+              v += dpp<0x124>(v);  // keys of a 16-lane row with this quarter
+              v += dpp<0x128>(v);
+              v += __shfl_xor(v, 16, 64);
+              v += __shfl_xor(v, 32, 64);
+              if (key == 0) sh[2 + quarter * 16 + e] = v;
+            }
+            if (lane == 0) {
+              sh[0] = m[h];
+              sh[1] = lt;
+            }
+          }
+        }
+      }
+      cbar(syp, gen, err);
+      STEP_MARK(l, 6);
+      // Merge the compute waves' states into this item's partial of each
+      // query head (wave h % 7 takes head h; lane = head dimension) and
+      // publish it.  With more splits than the O-phase consumers merge,
+      // split 0 then combines all splits of the head (its own included, read
+      // back like the others) into the final output.
+      {
+        const unsigned e1 = ep_of(E0, l, 1);
+        for (int h = cw; h < G; h += kNC) {
+          float M = -INFINITY;
+          for (int w = 0; w < kNC; ++w) M = fmaxf(M, st[((size_t)w * G + h) * kStRow]);
+          float Ls = 0.f, O = 0.f;
+          for (int w = 0; w < kNC; ++w) {
+            const float* sh = st + ((size_t)w * G + h) * kStRow;
+            const float f = exp2f(sh[0] - M);
+            Ls = fmaf(sh[1], f, Ls);
+            O = fmaf(sh[2 + lane], f, O);
+          }
+          O /= Ls;
+          const int j = j0 + h;
+          unsigned long long* pp = P.ll_part + ((size_t)j * s_cap + pl.it_sp) * 66;
+          // Partial = (log2 weight lambda = M + log2 Ls, normalised o): the
+          // splits of a head combine as a softmax over lambda.
+          ll_put(pp + 2 + lane, O, e1);
+          if (lane == 0) ll_put(pp, M + log2f(Ls), e1);  // written last: consumers poll it first
+          if (!pl.consumer_comb && pl.it_sp == 0) {
+            const unsigned long long* pj = P.ll_part + (size_t)j * s_cap * 66;
+            float Lm = -INFINITY, Ws = 0.f, Oc = 0.f;
+            for (int r0 = 0; r0 < pl.nspl; r0 += 8) {
+              unsigned long long w[8][2];
+              unsigned stale = 0;
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                const int i = r0 + u;
+                w[u][0] = w[u][1] = (unsigned long long)e1 << 32;
+                if (i < pl.nspl) {
+                  const unsigned long long* q0 = pj + (size_t)i * 66;
+                  w[u][0] = ll_get(q0);
+                  w[u][1] = ll_get(q0 + 2 + lane);
+                }
+                stale |= ((unsigned)(w[u][0] >> 32) != e1 || (unsigned)(w[u][1] >> 32) != e1 ? 1u : 0u) << u;
+              }
+              unsigned spins = 0;
+              unsigned long long t0 = 0;
+              while (stale) {
+                __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                  if (stale & (1u << u)) {
+                    const unsigned long long* q0 = pj + (size_t)(r0 + u) * 66;
+                    w[u][0] = ll_get(q0);
+                    w[u][1] = ll_get(q0 + 2 + lane);
+                    if ((unsigned)(w[u][0] >> 32) == e1 && (unsigned)(w[u][1] >> 32) == e1) stale &= ~(1u << u);
+                  }
+                if (stale && give_up(spins, t0, syp, err)) break;
+              }
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                if (r0 + u < pl.nspl) {
+                  const float lam = __uint_as_float((unsigned)w[u][0]);
+                  const float oi = __uint_as_float((unsigned)w[u][1]);
+                  const float Mn = fmaxf(Lm, lam);
+                  const float fa = exp2f(Lm - Mn), fb = exp2f(lam - Mn);
+                  Oc = Oc * fa + oi * fb;
+                  Ws = Ws * fa + fb;
+                  Lm = Mn;
+                }
+              }
+            }
+            Oc /= Ws;
+            ll_put(P.ll_o + j * 64 + lane, Oc, ep_of(E0, l, 2));
+          }
+        }
+      }
+      STEP_MARK(l, 7);
+    }
+
+    // ---------------------------------------------------- O projection + residual
+    STEP_MARK(l, 8);
+    quiet(1);
+    if (pl.consumer_comb) {
+      // o[j] = softmax over the splits i of head j of lambda_i, applied to
+      // the splits' o_i.  Wave cw takes heads cw + kNC u; all of a wave's
+      // loads are issued before any wait.
+      constexpr int HPW = kHeadsPerWave;  // heads per wave and round
+      const unsigned e1 = ep_of(E0, l, 1);
+      const int nsp = pl.nspl;
+      for (int jr = cw; jr < hq; jr += kNC * HPW) {
+        unsigned long long w[HPW][kMaxConsumerSplits][2];
+        // First the lambda words only (one request per wave instruction),
+        // until every split of this wave's heads has published; then the
+        // head dimensions, re-polling any that are still stale.
+        unsigned stale = 0;
+#pragma unroll
+        for (int u = 0; u < HPW; ++u)
+#pragma unroll
+          for (int i = 0; i < kMaxConsumerSplits; ++i) {
+            const int j = jr + u * kNC;
+            w[u][i][0] = w[u][i][1] = (unsigned long long)e1 << 32;
+            if (j < hq && i < nsp) w[u][i][0] = ll_get(P.ll_part + ((size_t)j * s_cap + i) * 66);
+            stale |= ((unsigned)(w[u][i][0] >> 32) != e1 ? 1u : 0u) << (u * kMaxConsumerSplits + i);
+          }
+        if (P.trace && tid == 64 * kLoaders && jr == cw) P.trace[((size_t)wg * (L + 1) + l) * 32 + 29] = wall_clock64();
+        unsigned spins = 0;
+        unsigned long long t0 = 0;
+        while (stale) {
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int u = 0; u < HPW; ++u)
+#pragma unroll
+            for (int i = 0; i < kMaxConsumerSplits; ++i) {
+              const unsigned bit = 1u << (u * kMaxConsumerSplits + i);
+              if (stale & bit) {
+                w[u][i][0] = ll_get(P.ll_part + ((size_t)(jr + u * kNC) * s_cap + i) * 66);
+                if ((unsigned)(w[u][i][0] >> 32) == e1) stale &= ~bit;
+              }
+            }
+          if (stale && give_up(spins, t0, syp, err)) break;
+        }
+        if (P.trace && tid == 64 * kLoaders && jr == cw) P.trace[((size_t)wg * (L + 1) + l) * 32 + 30] = wall_clock64();
+#pragma unroll
+        for (int u = 0; u < HPW; ++u)
+#pragma unroll
+          for (int i = 0; i < kMaxConsumerSplits; ++i) {
+            const int j = jr + u * kNC;
+            if (j < hq && i < nsp) w[u][i][1] = ll_get(P.ll_part + ((size_t)j * s_cap + i) * 66 + 2 + lane);
+            stale |= ((unsigned)(w[u][i][1] >> 32) != e1 ? 1u : 0u) << (u * kMaxConsumerSplits + i);
+          }
+        while (stale) {
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int u = 0; u < HPW; ++u)
+#pragma unroll
+            for (int i = 0; i < kMaxConsumerSplits; ++i) {
+              const unsigned bit = 1u << (u * kMaxConsumerSplits + i);
+              if (stale & bit) {
+                w[u][i][1] = ll_get(P.ll_part + ((size_t)(jr + u * kNC) * s_cap + i) * 66 + 2 + lane);
+                if ((unsigned)(w[u][i][1] >> 32) == e1) stale &= ~bit;
+              }
+            }
+          if (stale && give_up(spins, t0, syp, err)) break;
+        }
+        if (P.trace && tid == 64 * kLoaders && jr == cw) P.trace[((size_t)wg * (L + 1) + l) * 32 + 31] = wall_clock64();
+#pragma unroll
+        for (int u = 0; u < HPW; ++u) {
+          const int j = jr + u * kNC;
+          if (j < hq) {
+            float M = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < kMaxConsumerSplits; ++i)
+              if (i < nsp) M = fmaxf(M, __uint_as_float((unsigned)w[u][i][0]));
+            float Ws = 0.f, O = 0.f;
+#pragma unroll
+            for (int i = 0; i < kMaxConsumerSplits; ++i)
+              if (i < nsp) {
+                const float f = exp2f(__uint_as_float((unsigned)w[u][i][0]) - M);
+                Ws += f;
+                O = fmaf(f, __uint_as_float((unsigned)w[u][i][1]), O);
+              }
+            xc[j * 64 + lane] = O / Ws;
+          }
+        }
+      }
+    } else {
+      poll_span<kPollX>(P.ll_o, hq * 64, ep_of(E0, l, 2), syp, err, [&](int i, float v) { xc[i] = v; });
+    }
+    cbar(syp, gen, err);
+    quiet(0);
+    STEP_MARK(l, 9);
+    run_rows(lbase + pl.o_o, pl.n_o, xc, hq * 64, nd);
+    cbar(syp, gen, err);
+    STEP_MARK(l, 10);
+    if (cw == 0) {
+      const unsigned e = ep_of(E0, l, 3);
+      for (int i = lane; i < nd; i += 64) {
         const float xn = xown[i] + res[i];
         xown[i] = xn;
-        ll_put(dst + rd0 + i, xn, e);
+        ll_put(P.ll_xa + pl.rd0 + i, xn, e);
       }
-    } else if (kind == PH_GU) {
-      const unsigned e = ep_of(E0, l, 4);
-      for (int i = tid; i < j1 - j0; i += kStepThreads) ll_put(P.ll_m + j0 + i, silu(res[i]) * res[(j1 - j0) + i], e);
-    } else {  // PH_HEAD: logits, argmax; workgroup 0 publishes the token
-      const int nv = v1 - v0;
-      unsigned long long best = 0ull;
-      for (int i = tid; i < nv; i += kStepThreads) {
-        const float v = res[i];
-        if (P.logits) P.logits[v0 + i] = v;
-        const unsigned long long k = argmax_key(v, (uint32_t)(v0 + i));
-        best = k > best ? k : best;
+    }
+    STEP_MARK(l, 11);
+
+    // ---------------------------------------------------- RMSNorm + gate/up + SwiGLU
+    STEP_MARK(l, 12);
+    inv = stage_norm(P.ll_xa, ep_of(E0, l, 3), lptr[l].mlp_norm, tr(l, 26));
+    STEP_MARK(l, 13);
+    const int nj = pl.j1 - pl.j0;
+    run_rows(lbase + pl.o_gu, pl.n_gu, xa, d, 2 * nj);
+    cbar(syp, gen, err);
+    STEP_MARK(l, 14);
+    // ---------------------------------------------------- down projection (split-K) + residual
+    // This workgroup owns SwiGLU outputs j0 .. j1 - 1, so it multiplies them
+    // by the same columns of Wdown (rows of Wdown^T): a partial of the whole
+    // output, no exchange of the SwiGLU vector.  Partials are summed per
+    // output row, in workgroup order, by the row's owner.
+    {
+      constexpr int E = 16 / (int)sizeof(TW), PE = 1024 / (int)sizeof(TW);
+      constexpr int RPS = rows_per_slot(NPD);
+      float acc[NPD * E];
+#pragma unroll
+      for (int i = 0; i < NPD * E; ++i) acc[i] = 0.f;
+      const int dbase = lbase + pl.o_down;
+      for (int k = cw; k < pl.n_down; k += kNC) {
+        const int n = dbase + k, pos = n % S;
+        wait_landed(syp, n, pos, err);
+        const char* slot = ring + (size_t)pos * kSlot;
+#pragma unroll
+        for (int r = 0; r < RPS; ++r) {
+          const int jl = k * RPS + r;
+          // Rows missing from the slot repeat its first row: weight 0.
+          const float mj = jl < nj ? silu(res[jl] * inv) * (res[nj + jl] * inv) : 0.f;
+#pragma unroll
+          for (int c = 0; c < NPD; ++c) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(slot + (r * NPD + c) * 1024 + lane * 16);
+            float wf[E];
+            widen16(w, wf, TW());
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[c * E + e] = fmaf(mj, wf[e], acc[c * E + e]);
+          }
+        }
+        release_slot(syp, pos, n);
+      }
+      // Sum the compute waves' partials (fixed order) and publish them.
+      float* red = xa;  // [kNC][d] over the staging buffers, idle now
+#pragma unroll
+      for (int c = 0; c < NPD; ++c)
+#pragma unroll
+        for (int e = 0; e < E; e += 4)
+          *reinterpret_cast<float4*>(red + (size_t)cw * d + c * PE + lane * E + e) =
+              make_float4(acc[c * E + e], acc[c * E + e + 1], acc[c * E + e + 2], acc[c * E + e + 3]);
+      cbar(syp, gen, err);
+      STEP_MARK(l, 15);
+      {
+        const unsigned e4 = ep_of(E0, l, 4);
+        for (int i = tid - 64 * kLoaders; i < d; i += kNC * 64) {
+          float v = 0.f;
+#pragma unroll
+          for (int w = 0; w < kNC; ++w) v += red[(size_t)w * d + i];
+          ll_put(P.ll_dp + (size_t)wg * d + i, v, e4);
+        }
+      }
+      cbar(syp, gen, err);  // red is reused below
+      STEP_MARK(l, 16);
+      // Gather the partials of this workgroup's rows from every workgroup.
+      quiet(1);
+      {
+        const unsigned long long* dp = P.ll_dp + pl.rd0;
+        const int ndd = nd > 0 ? nd : 1;
+        poll_words<kPollX>([=](int i) { return dp + (size_t)(i / ndd) * d + (i % ndd); }, nwg * nd,
+                           ep_of(E0, l, 4), syp, err, [&](int i, float v) { red[i] = v; }, tr(l, 28));
+      }
+      cbar(syp, gen, err);
+      quiet(0);
+      STEP_MARK(l, 17);
+      // Row r of this workgroup: 32 lanes sum workgroups q, q + 32, ...;
+      // then the 32 lanes combine (a fixed reduction tree).
+      {
+        const unsigned e5 = ep_of(E0, l, 5);
+        for (int t0 = 0; t0 < nd * 32; t0 += kNC * 64) {
+          const int t = t0 + tid - 64 * kLoaders, r = t >> 5, q = t & 31;
+          float v = 0.f;
+          if (r < nd)
+            for (int w = q; w < nwg; w += 32) v += red[w * nd + r];
+          v = row_sum16(v);
+          v += __shfl_xor(v, 16, 64);
+          if (q == 0 && r < nd) {
+            const float xn = xown[r] + v;
+            xown[r] = xn;
+            ll_put(P.ll_xb + pl.rd0 + r, xn, e5);
+          }
+        }
+      }
+      STEP_MARK(l, 19);
+    }
+  }
+
+  // ---------------------------------------------------- final RMSNorm + LM head + argmax
+  STEP_MARK(L, 0);
+  inv = stage_norm(L == 0 ? nullptr : P.ll_xb, ep_of(E0, L - 1, 5), P.final_norm, tr(L, 24));
+  STEP_MARK(L, 1);
+  const int nv = pl.v1 - pl.v0;
+  run_rows(L * pl.per_layer, pl.head_slots, xa, d, nv);
+  cbar(syp, gen, err);
+  STEP_MARK(L, 2);
+  if (cw == 0) {
+    unsigned long long best = 0ull;
+    for (int i = lane; i < nv; i += 64) {
+      const float v = res[i] * inv;
+      if (P.logits) P.logits[pl.v0 + i] = v;
+      const unsigned long long k = argmax_key(v, (uint32_t)(pl.v0 + i));
+      best = k > best ? k : best;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const unsigned long long o2 = __shfl_xor(best, off, 64);
+      best = o2 > best ? o2 : best;
+    }
+    const unsigned e6 = ep_of(E0, L, 6);
+    if (lane == 0) {
+      ll_put_u(P.ll_keys + 2 * wg, (unsigned)(best >> 32), e6);
+      ll_put_u(P.ll_keys + 2 * wg + 1, (unsigned)best, e6);
+    }
+    if (wg == 0) {
+      unsigned long long b = 0ull;
+      for (int i0 = 0; i0 < nwg; i0 += 64) {
+        const int i = i0 + lane;
+        unsigned long long hi = (unsigned long long)e6 << 32, lo = hi;
+        if (i < nwg) {
+          hi = ll_get(P.ll_keys + 2 * i);
+          lo = ll_get(P.ll_keys + 2 * i + 1);
+        }
+        unsigned spins = 0;
+        unsigned long long t0 = 0;
+        while (__any((unsigned)(hi >> 32) != e6 || (unsigned)(lo >> 32) != e6)) {
+          __builtin_amdgcn_s_sleep(1);
+          if ((unsigned)(hi >> 32) != e6) hi = ll_get(P.ll_keys + 2 * i);
+          if ((unsigned)(lo >> 32) != e6) lo = ll_get(P.ll_keys + 2 * i + 1);
+          if (give_up(spins, t0, syp, err)) break;
+        }
+        if (i < nwg) {
+          const unsigned long long k = ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
+          b = k > b ? k : b;
+        }
       }
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
-        const unsigned long long o2 = __shfl_xor(best, off, 64);
-        best = o2 > best ? o2 : best;
+        const unsigned long long o2 = __shfl_xor(b, off, 64);
+        b = o2 > b ? o2 : b;
       }
-      if (lane == 0) kred[wave] = best;
-      __syncthreads();
-      const unsigned e6 = ep_of(E0, L, 6);
-      if (tid == 0) {
-        for (int w = 1; w < kStepWaves; ++w) best = kred[w] > best ? kred[w] : best;
-        ll_put_u(P.ll_keys + 2 * wg, (unsigned)(best >> 32), e6);
-        ll_put_u(P.ll_keys + 2 * wg + 1, (unsigned)best, e6);
-      }
-      if (wg == 0 && wave == 0) {
-        unsigned long long b = 0ull;
-        for (int i = lane; i < nwg; i += 64) {
-          const unsigned hi = ll_wait(P.ll_keys + 2 * i, e6, ll_get(P.ll_keys + 2 * i), P.err);
-          const unsigned lo = ll_wait(P.ll_keys + 2 * i + 1, e6, ll_get(P.ll_keys + 2 * i + 1), P.err);
-          const unsigned long long k = ((unsigned long long)hi << 32) | lo;
-          b = k > b ? k : b;
-        }
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-          const unsigned long long o2 = __shfl_xor(b, off, 64);
-          b = o2 > b ? o2 : b;
-        }
-        if (lane == 0) {
-          STEP_MARK(L, 15);
-          const int nt = argmax_index(b);
-          P.pending[s] = nt;
-          P.hist[(size_t)s * P.max_ctx + p] = nt;
-          P.pos[s] = p + 1;
-        }
+      if (lane == 0) {
+        const int nt = argmax_index(b);
+        P.pending[s] = nt;
+        P.hist[(size_t)s * P.max_ctx + p] = nt;
+        P.pos[s] = p + 1;
       }
     }
-
-    STEP_MARK(l, 17 + kind);
-    // ---- first weight batch of the next phase (it streams during the wait)
-    if (ip + 1 < nphase) {
-      const int l2 = ip + 1 == 4 * L ? L : (ip + 1) >> 2;
-      const int k2 = ip + 1 == 4 * L ? PH_HEAD : (ip + 1) & 3;
-      if (!(k2 == PH_O && has_item)) issue_first(l2, k2);
-    }
-    STEP_MARK(l, 22 + kind);
+    STEP_MARK(L, 3);
   }
+  (void)kred;
 }
 
 // ---------------------------------------------------------------- launcher
 
 template <typename TW, typename TKV>
-size_t StepKernel<TW, TKV>::lds_bytes(int d, int F, int hq) {
-  const int stage = d > F ? (d > hq * 64 ? d : hq * 64) : (F > hq * 64 ? F : hq * 64);
-  return (size_t)(stage + 2 * kStepResFloats + kStepWaves * 4 * 66 + kStepWaves * 64 + 128) * sizeof(float) +
-         kKvStageBytes;
+int StepKernel<TW, TKV>::xc_floats(int d, int F, int hq, int hkv) {
+  return step_xc_floats(d, hq, hkv);
 }
 
-template <typename TW, typename TKV, int CHD, int CHF>
+template <typename TW, typename TKV>
+size_t StepKernel<TW, TKV>::lds_bytes(int d, int F, int hq, int hkv, int ring_slots) {
+  return (size_t)ring_slots * kSlot + (size_t)(d + xc_floats(d, F, hq, hkv) + 2 * kStepResFloats) * sizeof(float);
+}
+
+// Pieces (1 KiB) per weight row for the row lengths d and F.
+template <typename TW>
+constexpr int pieces(int k) {
+  return (k * (int)sizeof(TW) + 1023) / 1024;
+}
+
+template <typename TW, typename TKV, int NPD, bool FD>
 static hipError_t launch_step(const StepParams<TW, TKV>& P, int nwg, hipStream_t st) {
-  const size_t lds = StepKernel<TW, TKV>::lds_bytes(P.d, P.F, P.hq);
-  auto kern = k_decode_step<TW, TKV, CHD, CHF>;
+  const size_t lds = StepKernel<TW, TKV>::lds_bytes(P.d, P.F, P.hq, P.hkv, P.ring_slots);
+  auto kern = k_decode_step<TW, TKV, NPD, FD>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -800,36 +1386,45 @@ static hipError_t launch_step(const StepParams<TW, TKV>& P, int nwg, hipStream_t
   return hipGetLastError();
 }
 
+// Instantiated row shapes (every streamed row has d elements): bf16 rows of
+// exactly 4 pieces (d = 2048), fp32 rows of exactly 1 piece (d = 256).
+template <typename TW>
+static bool shape_ok(int d, int F) {
+  (void)F;
+  if (sizeof(TW) == 2) return d * 2 == 4 * 1024;
+  return d * 4 == 1024;
+}
+
 template <typename TW, typename TKV>
 bool StepKernel<TW, TKV>::supports(int d, int F, int hq, int hkv, int V, int n_layers, int nwg) {
-  constexpr int Vn = Vec16<TW>::n;
-  const int chd = (d + 64 * Vn - 1) / (64 * Vn), chf = (F + 64 * Vn - 1) / (64 * Vn);
-  if (hq * 64 != d || hq % hkv || hq / hkv > kStepWaves || nwg / hkv < 1 || n_layers > kStepMaxLayers) return false;
-  if (d > kNormRegs * kStepThreads) return false;
+  if (!shape_ok<TW>(d, F)) return false;
+  const int G = hq / hkv;
+  if (hq * 64 != d || hq % hkv || G > kMaxGroup || nwg / hkv < 1 || n_layers > kStepMaxLayers) return false;
+  if (sizeof(TKV) == 4 && G > kMaxGroupF32) return false;
   const int pairs = (hq + 2 * hkv) * 32;
-  if ((V + nwg - 1) / nwg > kStepResFloats || 2 * ((F + nwg - 1) / nwg) > kStepResFloats ||
-      2 * ((pairs + nwg - 1) / nwg) > kStepResFloats || (d + nwg - 1) / nwg > kStepResFloats)
+  // Row results per phase (gate/up shares grow by at most the item rebalancing).
+  if ((V + nwg - 1) / nwg > kStepResFloats || 2 * ((F + nwg - 1) / nwg) + 64 > kStepResFloats ||
+      2 * ((pairs + nwg - 1) / nwg) > kStepResFloats || 2 * ((d + nwg - 1) / nwg) > kStepResFloats)
     return false;
-  if (lds_bytes(d, F, hq) > 144 * 1024) return false;  // plus ~12 KiB of static LDS
-  if (sizeof(TW) == 2) return chd <= 4 && chf <= 16;
-  return chd <= 1 && chf <= 3;
+  if (lds_bytes(d, F, hq, hkv, kStepRingSlots) > 148 * 1024) return false;  // plus the static LDS
+  return true;
 }
 
 template <typename TW, typename TKV>
 hipError_t StepKernel<TW, TKV>::launch(const StepParams<TW, TKV>& P, int nwg, hipStream_t st) {
-  if constexpr (sizeof(TW) == 2) return launch_step<TW, TKV, 4, 16>(P, nwg, st);
-  else return launch_step<TW, TKV, 1, 3>(P, nwg, st);
+  if constexpr (sizeof(TW) == 2) return launch_step<TW, TKV, 4, true>(P, nwg, st);
+  else return launch_step<TW, TKV, 1, true>(P, nwg, st);
 }
 
 template <typename TW, typename TKV>
-int StepKernel<TW, TKV>::max_blocks_per_cu(int d, int F, int hq) {
-  const size_t lds = lds_bytes(d, F, hq);
+int StepKernel<TW, TKV>::max_blocks_per_cu(int d, int F, int hq, int hkv) {
+  const size_t lds = lds_bytes(d, F, hq, hkv, kStepRingSlots);
   int nb = 0;
   hipError_t e;
   if constexpr (sizeof(TW) == 2)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_decode_step<TW, TKV, 4, 16>, kStepThreads, lds);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_decode_step<TW, TKV, 4, true>, kStepThreads, lds);
   else
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_decode_step<TW, TKV, 1, 3>, kStepThreads, lds);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_decode_step<TW, TKV, 1, true>, kStepThreads, lds);
   return e == hipSuccess ? nb : 0;
 }
 

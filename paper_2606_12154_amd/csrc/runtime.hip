@@ -34,7 +34,7 @@ struct Layout {
   int nqkv, max_pages, n_pages, rows_cap, logit_rows;
   // byte offsets into the arena
   size_t embed, lm_head, embedM, lm_headM;
-  std::vector<size_t> wqkv, wo, wgu, wdown, wqkvM, woM, wguM, wdownM, attn_norm, mlp_norm;
+  std::vector<size_t> wqkv, wo, wgu, wdown, wdownT, wqkvM, woM, wguM, wdownM, attn_norm, mlp_norm;
   size_t final_norm, rope, kv, page_table, pos, pending, slot, hist, ll, ll_words, layer_tab, trace;
   size_t row_stream, row_pos, feed, x, h, q, qM, o32, oM, m32, mM, part, logits, gemm_ws, gemm_ws_bytes, scratch_u32;
   size_t total;
@@ -84,6 +84,7 @@ Layout make_layout(const hh_config& c) {
     L.wo.push_back(take(d * hq * 64 * L.ew));
     L.wgu.push_back(take(2 * F * d * L.ew));
     L.wdown.push_back(take(d * F * L.ew));
+    L.wdownT.push_back(take(d * F * L.ew));
   }
   if (bf) {
     L.embedM = take(V * d * L.em);
@@ -116,9 +117,10 @@ Layout make_layout(const hh_config& c) {
   L.hist = take((size_t)c.max_streams * c.max_context * 4);
   // Epoch-tagged exchange words of the persistent decode kernel (see k_step.hip):
   // xa, xb [d], q [Hq*64], kn, vn [Hkv*64], partials [Hq][kMaxStepWG][66],
-  // o [Hq*64], m [F], keys [2*kMaxStepWG], then the error flag.
-  L.ll_words = 2 * d + 2 * (size_t)hq * 64 + 2 * (size_t)c.n_kv_heads * 64 + (size_t)hq * kMaxStepWG * 66 + F +
-               2 * kMaxStepWG + 8;
+  // o [Hq*64], down partials [kMaxStepWG][d], keys [2*kMaxStepWG], then the
+  // error flag.
+  L.ll_words = 2 * d + 2 * (size_t)hq * 64 + 2 * (size_t)c.n_kv_heads * 64 + (size_t)hq * kMaxStepWG * 66 +
+               (size_t)kMaxStepWG * d + 2 * kMaxStepWG + 8;
   L.ll = take(L.ll_words * 8);
   L.layer_tab = take((size_t)c.n_layers * sizeof(LayerPtrs<float>));
   L.trace = take((size_t)kMaxStepWG * (c.n_layers + 1) * 32 * 8);  // optional phase timestamps
@@ -165,6 +167,8 @@ struct hh_ctx {
   float wscale = 1.f;  // MFMA weights hold w * wscale (fp16 repack); epilogues multiply by 1/wscale
   int step_wg = 0;     // workgroups of the persistent batch-1 decode kernel (0: not usable)
   unsigned step_count = 0;  // persistent-kernel launches so far (names each step's epochs)
+  int step_depth = kStepLoadDepth;  // HH_LOAD_DEPTH: ring slots in flight per streaming wave
+  int step_quiet = 0;               // HH_STEP_QUIET: pause streaming during exchange waits
   std::string trace_path;   // HH_STEP_TRACE: file receiving the last traced step's phase timestamps
   std::string err;
   // host mirror of the device bookkeeping
@@ -290,8 +294,10 @@ hipError_t setup_step_tables(hh_ctx* c) {
   const Layout& L = c->L;
   std::vector<LayerPtrs<TW>> tab(g.n_layers);
   for (int l = 0; l < g.n_layers; ++l)
-    tab[l] = LayerPtrs<TW>{c->at<TW>(L.wqkv[l]), c->at<TW>(L.wo[l]), c->at<TW>(L.wgu[l]), c->at<TW>(L.wdown[l]),
-                           c->at<float>(L.attn_norm[l]), c->at<float>(L.mlp_norm[l])};
+    tab[l] = LayerPtrs<TW>{c->at<TW>(L.wqkv[l]),      c->at<TW>(L.wo[l]),
+                           c->at<TW>(L.wgu[l]),       c->at<TW>(L.wdown[l]),
+                           c->at<TW>(L.wdownT[l]),    c->at<float>(L.attn_norm[l]),
+                           c->at<float>(L.mlp_norm[l])};
   if (g.n_layers == 0) return hipSuccess;
   hipError_t e = hipMemcpyAsync(c->arena + L.layer_tab, tab.data(), tab.size() * sizeof(LayerPtrs<TW>),
                                 hipMemcpyHostToDevice, c->stream);
@@ -309,8 +315,9 @@ int step_workgroups(const hh_config& g) {
   const int nwg = std::min(cus, kMaxStepWG);
   if (!StepKernel<TW, TKV>::supports(g.d_model, g.ffn_dim, g.n_heads, g.n_kv_heads, g.vocab, g.n_layers, nwg))
     return 0;
-  if ((g.max_context + kPage - 1) / kPage > kStepMaxItemPages) return 0;
-  if (StepKernel<TW, TKV>::max_blocks_per_cu(g.d_model, g.ffn_dim, g.n_heads) < 1) return 0;
+  // An attention item covers at most 256 pages (its page list sits in LDS).
+  if ((g.max_context + kPage - 1) / kPage > 256 * (nwg / g.n_kv_heads)) return 0;
+  if (StepKernel<TW, TKV>::max_blocks_per_cu(g.d_model, g.ffn_dim, g.n_heads, g.n_kv_heads) < 1) return 0;
   return nwg;
 }
 
@@ -336,7 +343,9 @@ hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
   P.n_layers = g.n_layers;
   P.max_ctx = g.max_context;
   P.stream = s;
-  P.stage_floats = std::max(std::max(g.d_model, g.ffn_dim), g.n_heads * 64);
+  P.ring_slots = kStepRingSlots;
+  P.load_depth = c->step_depth;
+  P.quiet = c->step_quiet;
   P.eps = g.rms_eps;
   // Each step owns 512 epochs (8 phases x 64 layers); epoch 0 is never used,
   // so the zero-initialised exchange words never look current.
@@ -364,8 +373,8 @@ hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
   P.ll_vn = P.ll_kn + hkv * 64;
   P.ll_part = P.ll_vn + hkv * 64;
   P.ll_o = P.ll_part + hq * kMaxStepWG * 66;
-  P.ll_m = P.ll_o + hq * 64;
-  P.ll_keys = P.ll_m + g.ffn_dim;
+  P.ll_dp = P.ll_o + hq * 64;
+  P.ll_keys = P.ll_dp + (size_t)kMaxStepWG * d;
   P.err = reinterpret_cast<int*>(P.ll_keys + 2 * kMaxStepWG);
   P.trace = c->trace_path.empty() ? nullptr : c->at<unsigned long long>(L.trace);
   const hipError_t e = StepKernel<TW, TKV>::launch(P, c->step_wg, c->stream);
@@ -538,6 +547,8 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   c->stream = static_cast<hipStream_t>(hip_stream);
   const char* tp = std::getenv("HH_STEP_TRACE");
   if (tp) c->trace_path = tp;
+  if (const char* q = std::getenv("HH_STEP_QUIET")) c->step_quiet = std::atoi(q);
+  if (const char* ld = std::getenv("HH_LOAD_DEPTH")) c->step_depth = std::min(7, std::max(1, std::atoi(ld)));
   const char* ge = std::getenv("HH_GRAPHS");
   c->use_graphs = !(ge && ge[0] == '0');
   c->len.assign(cfg->max_streams, 0);
@@ -601,6 +612,8 @@ hh_status hh_load_weights(hh_ctx* c, const void* const* tensors, int32_t n_tenso
     HIPCHK(c, copy(L.wgu[l], tensors[t++], F * d * L.ew));
     HIPCHK(c, copy(L.wgu[l] + F * d * L.ew, tensors[t++], F * d * L.ew));
     HIPCHK(c, copy(L.wdown[l], tensors[t++], d * F * L.ew));
+    if (bf) transpose(st, c->at<__bf16>(L.wdown[l]), c->at<__bf16>(L.wdownT[l]), (int)d, (int)F);
+    else transpose(st, c->at<float>(L.wdown[l]), c->at<float>(L.wdownT[l]), (int)d, (int)F);
   }
   HIPCHK(c, gain(L.final_norm, tensors[t++]));
   if (!g.tied_embeddings) HIPCHK(c, copy(L.lm_head, tensors[t++], V * d * L.ew));
