@@ -73,16 +73,24 @@ struct LayerPtrs {
   const float* mlp_norm;
 };
 
+// The batch-1 decode kernel streams the fp16 (x 2^s) copies of bf16 models'
+// matrices (one v_fma_mix per weight, no widening); the token embedding it
+// looks up stays in the model's own type.
+template <typename TW> struct StepEmbed { using type = TW; };
+template <> struct StepEmbed<_Float16> { using type = __bf16; };
+
 template <typename TW, typename TKV>
 struct StepParams {
   int d, F, hq, hkv, V, n_layers, max_ctx, stream;
   int ring_slots;              // LDS ring slots per workgroup (<= 16)
   int load_depth;              // ring slots each streaming wave keeps in flight (1 .. 7)
   int quiet;                   // 1: streaming pauses while compute waves wait for other workgroups
+  int poll_delay;              // ticks (10 ns) to wait before a phase's first exchange poll
   float eps;
   unsigned epoch;              // base epoch of this step (distinct for every step)
   const LayerPtrs<TW>* layer;  // device array [n_layers]
-  const TW* embed;
+  float wscale_inv;            // 1 / the power-of-two scale of the streamed matrices
+  const typename StepEmbed<TW>::type* embed;
   const TW* head;
   const float* final_norm;
   const float2* rope;

@@ -67,5 +67,6 @@ void transpose(hipStream_t st, const T* src, T* dst, int rows, int cols) {
 }
 template void transpose<__bf16>(hipStream_t, const __bf16*, __bf16*, int, int);
 template void transpose<float>(hipStream_t, const float*, float*, int, int);
+template void transpose<_Float16>(hipStream_t, const _Float16*, _Float16*, int, int);
 
 }  // namespace hh

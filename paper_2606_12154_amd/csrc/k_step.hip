@@ -268,9 +268,13 @@ __device__ __forceinline__ void slot_rows(const char* slot, const float* xs, int
     constexpr int LOG = log2_small(RPS);
     static_assert((1 << LOG) == RPS, "rows per slot must be a power of two");
     const int r0 = k * RPS;
-    float acc[RPS];
+    // One accumulator per (row, piece): independent FMA chains interleave
+    // instead of serialising on the FMA latency.
+    float acc[RPS][NP];
 #pragma unroll
-    for (int r = 0; r < RPS; ++r) acc[r] = 0.f;
+    for (int r = 0; r < RPS; ++r)
+#pragma unroll
+      for (int c = 0; c < NP; ++c) acc[r][c] = 0.f;
 #pragma unroll
     for (int c = 0; c < NP; ++c) {
       const int e0 = c * PE + lane * E;
@@ -290,14 +294,17 @@ __device__ __forceinline__ void slot_rows(const char* slot, const float* xs, int
         float wf[E];
         widen16(w, wf, TW());
 #pragma unroll
-        for (int e = 0; e < E; ++e) acc[r] = fmaf(ok ? wf[e] : 0.f, xv[e], acc[r]);
+        for (int e = 0; e < E; ++e) acc[r][c] = fmaf(ok ? wf[e] : 0.f, xv[e], acc[r][c]);
       }
     }
     // Row totals by DPP row sums and lane reads (VALU only: a chain of
     // LDS-routed shuffles would dominate the latency of a small phase).
 #pragma unroll
     for (int r = 0; r < RPS; ++r) {
-      const float tot = wave_sum_u(acc[r]);
+      float a = 0.f;
+#pragma unroll
+      for (int c = 0; c < NP; ++c) a += acc[r][c];
+      const float tot = wave_sum_u(a);
       if (lane == 0 && r0 + r < n_rows) res[r0 + r] = tot;
     }
   } else {
@@ -402,9 +409,10 @@ __device__ __forceinline__ void make_plan(Plan& pl, const StepParams<TW, TKV>& P
   pl.it_pg1 = pl.it_pg0 + per < npg ? pl.it_pg0 + per : npg;
   pl.consumer_comb = nspl <= kMaxConsumerSplits;
   // SwiGLU outputs: item workgroups take fewer, so every workgroup streams
-  // about the same bytes per layer.  A gate/up output is two d-rows.
+  // about the same bytes per layer.  An output is three d-rows (gate, up,
+  // and the Wdown^T row it multiplies).
   const int kv_slots = (per + pps - 1) / pps;
-  const int gu_unit = 2 * NPD * 1024;  // bytes of one output's rows
+  const int gu_unit = 3 * NPD * 1024;  // bytes of one output's rows: gate, up and its Wdown^T row
   int kvu = (kv_slots * kSlot + gu_unit / 2) / gu_unit;
   long long tot = (long long)F + (long long)pl.n_items * kvu;
   if (tot < (long long)kvu * nwg) {  // items would get a negative share: plain split
@@ -532,7 +540,8 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
   if (pl.has_item)
     for (int i = tid; i < pl.it_pg1 - pl.it_pg0; i += kStepThreads)
       item_pages[i] = P.page_table[(size_t)s * P.kv.max_pages + pl.it_pg0 + i];
-  const TW* erow = P.embed + (size_t)tok * d;
+  const typename StepEmbed<TW>::type* erow = P.embed + (size_t)tok * d;
+  const float ws = P.wscale_inv;
   for (int i = tid; i < nd; i += kStepThreads) xown[i] = (float)erow[pl.rd0 + i];
   const int page_p = P.page_table[(size_t)s * P.kv.max_pages + p / kPage];  // page receiving this position
   __syncthreads();
@@ -696,6 +705,15 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
 
   // Stage x (words at epoch ep, or the embedding row when src is null) times
   // the RMSNorm gain into xa; returns 1 / rms after a compute-wave barrier.
+  // Optional delay before a phase's first poll (ticks of the 100 MHz clock):
+  // a poll issued before the last producer's words are visible costs a full
+  // extra round trip.
+  auto poll_delay = [&](int ticks) {
+    if (ticks > 0) {
+      const unsigned long long t_end = wall_clock64() + (unsigned)ticks;
+      while (wall_clock64() < t_end) __builtin_amdgcn_s_sleep(1);
+    }
+  };
   auto quiet = [&](int on) {
     if (cw == 0 && lane == 0) *(volatile int HH_LDS*)&syp->quiet = on;
   };
@@ -704,6 +722,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
   };
   auto stage_norm = [&](const unsigned long long* src, unsigned ep, const float* gain, PollTrace pt) -> float {
     quiet(1);
+    if (src) poll_delay(P.poll_delay);
     float ss = 0.f;
     const int tc = tid - 64 * kLoaders;
     if (src) {
@@ -769,7 +788,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
       const unsigned e = ep_of(E0, l, 0);
       for (int lp = lane; lp < pl.pq1 - pl.pq0; lp += 64) {
         const int gp = pl.pq0 + lp, head = gp >> 5, i = gp & 31;
-        const float y0 = res[2 * lp] * inv, y1 = res[2 * lp + 1] * inv;
+        const float y0 = res[2 * lp] * (inv * ws), y1 = res[2 * lp + 1] * (inv * ws);
         if (head < hq + hkv) {
           const float2 cs = rope_p[i];
           const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
@@ -1037,8 +1056,8 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
           unsigned long long* pp = P.ll_part + ((size_t)j * s_cap + pl.it_sp) * 66;
           // Partial = (log2 weight lambda = M + log2 Ls, normalised o): the
           // splits of a head combine as a softmax over lambda.
+          if (lane == 0) ll_put(pp, M + log2f(Ls), e1);
           ll_put(pp + 2 + lane, O, e1);
-          if (lane == 0) ll_put(pp, M + log2f(Ls), e1);  // written last: consumers poll it first
           if (!pl.consumer_comb && pl.it_sp == 0) {
             const unsigned long long* pj = P.ll_part + (size_t)j * s_cap * 66;
             float Lm = -INFINITY, Ws = 0.f, Oc = 0.f;
@@ -1094,6 +1113,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
     // ---------------------------------------------------- O projection + residual
     STEP_MARK(l, 8);
     quiet(1);
+    poll_delay(P.poll_delay);
     if (pl.consumer_comb) {
       // o[j] = softmax over the splits i of head j of lambda_i, applied to
       // the splits' o_i.  Wave cw takes heads cw + kNC u; all of a wave's
@@ -1103,9 +1123,6 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
       const int nsp = pl.nspl;
       for (int jr = cw; jr < hq; jr += kNC * HPW) {
         unsigned long long w[HPW][kMaxConsumerSplits][2];
-        // First the lambda words only (one request per wave instruction),
-        // until every split of this wave's heads has published; then the
-        // head dimensions, re-polling any that are still stale.
         unsigned stale = 0;
 #pragma unroll
         for (int u = 0; u < HPW; ++u)
@@ -1113,10 +1130,14 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
           for (int i = 0; i < kMaxConsumerSplits; ++i) {
             const int j = jr + u * kNC;
             w[u][i][0] = w[u][i][1] = (unsigned long long)e1 << 32;
-            if (j < hq && i < nsp) w[u][i][0] = ll_get(P.ll_part + ((size_t)j * s_cap + i) * 66);
-            stale |= ((unsigned)(w[u][i][0] >> 32) != e1 ? 1u : 0u) << (u * kMaxConsumerSplits + i);
+            if (j < hq && i < nsp) {
+              const unsigned long long* q0 = P.ll_part + ((size_t)j * s_cap + i) * 66;
+              w[u][i][0] = ll_get(q0);
+              w[u][i][1] = ll_get(q0 + 2 + lane);
+            }
+            stale |= ((unsigned)(w[u][i][0] >> 32) != e1 || (unsigned)(w[u][i][1] >> 32) != e1 ? 1u : 0u)
+                     << (u * kMaxConsumerSplits + i);
           }
-        if (P.trace && tid == 64 * kLoaders && jr == cw) P.trace[((size_t)wg * (L + 1) + l) * 32 + 29] = wall_clock64();
         unsigned spins = 0;
         unsigned long long t0 = 0;
         while (stale) {
@@ -1127,36 +1148,14 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
             for (int i = 0; i < kMaxConsumerSplits; ++i) {
               const unsigned bit = 1u << (u * kMaxConsumerSplits + i);
               if (stale & bit) {
-                w[u][i][0] = ll_get(P.ll_part + ((size_t)(jr + u * kNC) * s_cap + i) * 66);
-                if ((unsigned)(w[u][i][0] >> 32) == e1) stale &= ~bit;
+                const unsigned long long* q0 = P.ll_part + ((size_t)(jr + u * kNC) * s_cap + i) * 66;
+                w[u][i][0] = ll_get(q0);
+                w[u][i][1] = ll_get(q0 + 2 + lane);
+                if ((unsigned)(w[u][i][0] >> 32) == e1 && (unsigned)(w[u][i][1] >> 32) == e1) stale &= ~bit;
               }
             }
           if (stale && give_up(spins, t0, syp, err)) break;
         }
-        if (P.trace && tid == 64 * kLoaders && jr == cw) P.trace[((size_t)wg * (L + 1) + l) * 32 + 30] = wall_clock64();
-#pragma unroll
-        for (int u = 0; u < HPW; ++u)
-#pragma unroll
-          for (int i = 0; i < kMaxConsumerSplits; ++i) {
-            const int j = jr + u * kNC;
-            if (j < hq && i < nsp) w[u][i][1] = ll_get(P.ll_part + ((size_t)j * s_cap + i) * 66 + 2 + lane);
-            stale |= ((unsigned)(w[u][i][1] >> 32) != e1 ? 1u : 0u) << (u * kMaxConsumerSplits + i);
-          }
-        while (stale) {
-          __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-          for (int u = 0; u < HPW; ++u)
-#pragma unroll
-            for (int i = 0; i < kMaxConsumerSplits; ++i) {
-              const unsigned bit = 1u << (u * kMaxConsumerSplits + i);
-              if (stale & bit) {
-                w[u][i][1] = ll_get(P.ll_part + ((size_t)(jr + u * kNC) * s_cap + i) * 66 + 2 + lane);
-                if ((unsigned)(w[u][i][1] >> 32) == e1) stale &= ~bit;
-              }
-            }
-          if (stale && give_up(spins, t0, syp, err)) break;
-        }
-        if (P.trace && tid == 64 * kLoaders && jr == cw) P.trace[((size_t)wg * (L + 1) + l) * 32 + 31] = wall_clock64();
 #pragma unroll
         for (int u = 0; u < HPW; ++u) {
           const int j = jr + u * kNC;
@@ -1189,7 +1188,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
     if (cw == 0) {
       const unsigned e = ep_of(E0, l, 3);
       for (int i = lane; i < nd; i += 64) {
-        const float xn = xown[i] + res[i];
+        const float xn = xown[i] + res[i] * ws;
         xown[i] = xn;
         ll_put(P.ll_xa + pl.rd0 + i, xn, e);
       }
@@ -1224,7 +1223,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
         for (int r = 0; r < RPS; ++r) {
           const int jl = k * RPS + r;
           // Rows missing from the slot repeat its first row: weight 0.
-          const float mj = jl < nj ? silu(res[jl] * inv) * (res[nj + jl] * inv) : 0.f;
+          const float mj = jl < nj ? silu(res[jl] * (inv * ws)) * (res[nj + jl] * (inv * ws)) : 0.f;
 #pragma unroll
           for (int c = 0; c < NPD; ++c) {
             const u32x4 w = *reinterpret_cast<const u32x4*>(slot + (r * NPD + c) * 1024 + lane * 16);
@@ -1252,13 +1251,14 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
           float v = 0.f;
 #pragma unroll
           for (int w = 0; w < kNC; ++w) v += red[(size_t)w * d + i];
-          ll_put(P.ll_dp + (size_t)wg * d + i, v, e4);
+          ll_put(P.ll_dp + (size_t)wg * d + i, v * ws, e4);
         }
       }
       cbar(syp, gen, err);  // red is reused below
       STEP_MARK(l, 16);
       // Gather the partials of this workgroup's rows from every workgroup.
       quiet(1);
+      poll_delay(P.poll_delay);
       {
         const unsigned long long* dp = P.ll_dp + pl.rd0;
         const int ndd = nd > 0 ? nd : 1;
@@ -1301,7 +1301,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
   if (cw == 0) {
     unsigned long long best = 0ull;
     for (int i = lane; i < nv; i += 64) {
-      const float v = res[i] * inv;
+      const float v = res[i] * (inv * ws);
       if (P.logits) P.logits[pl.v0 + i] = v;
       const unsigned long long k = argmax_key(v, (uint32_t)(pl.v0 + i));
       best = k > best ? k : best;
@@ -1428,7 +1428,7 @@ int StepKernel<TW, TKV>::max_blocks_per_cu(int d, int F, int hq, int hkv) {
   return e == hipSuccess ? nb : 0;
 }
 
-template struct StepKernel<__bf16, _Float16>;
+template struct StepKernel<_Float16, _Float16>;
 template struct StepKernel<float, float>;
 
 }  // namespace hh

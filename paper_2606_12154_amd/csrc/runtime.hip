@@ -169,6 +169,8 @@ struct hh_ctx {
   unsigned step_count = 0;  // persistent-kernel launches so far (names each step's epochs)
   int step_depth = kStepLoadDepth;  // HH_LOAD_DEPTH: ring slots in flight per streaming wave
   int step_quiet = 0;               // HH_STEP_QUIET: pause streaming during exchange waits
+  int step_ring = kStepRingSlots;   // HH_RING_SLOTS: LDS ring slots used (at most kStepRingSlots)
+  int step_poll_delay = 60;         // HH_POLL_DELAY: 10 ns ticks before a phase's first exchange poll
   std::string trace_path;   // HH_STEP_TRACE: file receiving the last traced step's phase timestamps
   std::string err;
   // host mirror of the device bookkeeping
@@ -294,8 +296,8 @@ hipError_t setup_step_tables(hh_ctx* c) {
   const Layout& L = c->L;
   std::vector<LayerPtrs<TW>> tab(g.n_layers);
   for (int l = 0; l < g.n_layers; ++l)
-    tab[l] = LayerPtrs<TW>{c->at<TW>(L.wqkv[l]),      c->at<TW>(L.wo[l]),
-                           c->at<TW>(L.wgu[l]),       c->at<TW>(L.wdown[l]),
+    tab[l] = LayerPtrs<TW>{c->at<TW>(L.wqkvM[l]),     c->at<TW>(L.woM[l]),
+                           c->at<TW>(L.wguM[l]),      c->at<TW>(L.wdownM[l]),
                            c->at<TW>(L.wdownT[l]),    c->at<float>(L.attn_norm[l]),
                            c->at<float>(L.mlp_norm[l])};
   if (g.n_layers == 0) return hipSuccess;
@@ -323,8 +325,8 @@ int step_workgroups(const hh_config& g) {
 
 hipError_t setup_step_kernel(hh_ctx* c) {
   if (c->cfg.dtype == HH_BF16) {
-    c->step_wg = step_workgroups<__bf16, _Float16>(c->cfg);
-    return setup_step_tables<__bf16>(c);
+    c->step_wg = step_workgroups<_Float16, _Float16>(c->cfg);
+    return setup_step_tables<_Float16>(c);
   }
   c->step_wg = step_workgroups<float, float>(c->cfg);
   return setup_step_tables<float>(c);
@@ -343,17 +345,19 @@ hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
   P.n_layers = g.n_layers;
   P.max_ctx = g.max_context;
   P.stream = s;
-  P.ring_slots = kStepRingSlots;
+  P.ring_slots = c->step_ring;
   P.load_depth = c->step_depth;
   P.quiet = c->step_quiet;
+  P.poll_delay = c->step_poll_delay;
   P.eps = g.rms_eps;
   // Each step owns 512 epochs (8 phases x 64 layers); epoch 0 is never used,
   // so the zero-initialised exchange words never look current.
   c->step_count += 1;
   P.epoch = c->step_count * 512u;
   P.layer = c->at<LayerPtrs<TW>>(L.layer_tab);
-  P.embed = c->at<TW>(L.embed);
-  P.head = c->at<TW>(L.lm_head);
+  P.embed = c->at<typename StepEmbed<TW>::type>(L.embed);
+  P.head = c->at<TW>(L.lm_headM);
+  P.wscale_inv = 1.0f / c->wscale;
   P.final_norm = c->at<float>(L.final_norm);
   P.rope = c->at<float2>(L.rope);
   P.kvc = c->at<TKV>(L.kv);
@@ -459,7 +463,7 @@ hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t
   if (tokens) HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, n * sizeof(int), hipMemcpyHostToDevice, st));
   const bool want_logits = logits != nullptr;
   if (n == 1 && c->step_wg > 0) {
-    hh_status rc = launch_step<TW, TKV>(c, ids[0], tokens != nullptr, want_logits);
+    hh_status rc = launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits);
     if (rc != HH_OK) return rc;
   } else if (c->use_graphs) {
     auto key = std::make_tuple(n, tokens != nullptr ? 1 : 0, want_logits ? 1 : 0);
@@ -548,6 +552,8 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   const char* tp = std::getenv("HH_STEP_TRACE");
   if (tp) c->trace_path = tp;
   if (const char* q = std::getenv("HH_STEP_QUIET")) c->step_quiet = std::atoi(q);
+  if (const char* pd = std::getenv("HH_POLL_DELAY")) c->step_poll_delay = std::max(0, std::atoi(pd));
+  if (const char* r = std::getenv("HH_RING_SLOTS")) c->step_ring = std::min(kStepRingSlots, std::max(6, std::atoi(r)));
   if (const char* ld = std::getenv("HH_LOAD_DEPTH")) c->step_depth = std::min(7, std::max(1, std::atoi(ld)));
   const char* ge = std::getenv("HH_GRAPHS");
   c->use_graphs = !(ge && ge[0] == '0');
@@ -612,8 +618,7 @@ hh_status hh_load_weights(hh_ctx* c, const void* const* tensors, int32_t n_tenso
     HIPCHK(c, copy(L.wgu[l], tensors[t++], F * d * L.ew));
     HIPCHK(c, copy(L.wgu[l] + F * d * L.ew, tensors[t++], F * d * L.ew));
     HIPCHK(c, copy(L.wdown[l], tensors[t++], d * F * L.ew));
-    if (bf) transpose(st, c->at<__bf16>(L.wdown[l]), c->at<__bf16>(L.wdownT[l]), (int)d, (int)F);
-    else transpose(st, c->at<float>(L.wdown[l]), c->at<float>(L.wdownT[l]), (int)d, (int)F);
+    if (!bf) transpose(st, c->at<float>(L.wdown[l]), c->at<float>(L.wdownT[l]), (int)d, (int)F);
   }
   HIPCHK(c, gain(L.final_norm, tensors[t++]));
   if (!g.tied_embeddings) HIPCHK(c, copy(L.lm_head, tensors[t++], V * d * L.ew));
@@ -643,6 +648,9 @@ hh_status hh_load_weights(hh_ctx* c, const void* const* tensors, int32_t n_tenso
     for (auto& m : list)
       bf16_to_f16_scaled(st, c->at<__bf16>(std::get<0>(m)), c->at<_Float16>(std::get<1>(m)), std::get<2>(m),
                          c->wscale);
+    // Wdown^T of the fp16 copy, for the batch-1 decode kernel's split-K down projection.
+    for (int l = 0; l < g.n_layers; ++l)
+      transpose(st, c->at<_Float16>(L.wdownM[l]), c->at<_Float16>(L.wdownT[l]), (int)d, (int)F);
   } else {
     c->wscale = 1.f;
   }
