@@ -1,17 +1,20 @@
 // Causal GQA flash attention for prompt prefill on gfx950 MFMA (fp16 KV).
 //
-// A workgroup owns one block of 32 query positions and one kv head g; wave w
-// serves query head g * G + w.  Per block of 32 keys (two KV pages):
+// A workgroup owns one block of 32 query positions and one kv head g.  Its
+// waves form NS key-split groups of G waves; wave w of a group serves query
+// head g * G + w, and group s takes key blocks s, s + NS, s + 2 NS, ... of 32
+// keys (two KV pages), so the longest dependency chain is 1/NS of the keys and
+// every SIMD runs four waves that hide each other's latencies.  Per key block:
 //   S^T[key][query] = K[key][:] . Q[query][:]      4 x mfma_f32_32x32x16_f16
 // so a lane holds 16 keys of ONE query column (lane % 32), and the row max /
 // sum of the online softmax need a single exchange with lane ^ 32.  Then
 //   O^T[dim][query] += V^T[dim][key] P^T[key][query]   4 x mfma 32x32x16
 // where the second contraction's K index is ordered to match the keys each
 // lane already holds in S^T (j -> key 16t + 8(j/4) + 4h + j%4 for lane half h),
-// so P goes from the accumulator straight into the B operand.  K and V^T of
-// a key block are staged once per workgroup in LDS (all waves read them), so
-// each lane's K operand is one 16-byte read and its V^T operand two 8-byte
-// reads.
+// so P goes from the accumulator straight into the B operand.  K and V^T of a
+// key block are staged once per group in LDS (the group's waves all read
+// them).  At the end the groups' (max, sum, output) triples are merged in LDS
+// by group 0 in split order.
 // Result lane layout of a 32x32 MFMA: element i of lane l is row
 // 8(i/4) + 4(l/32) + i%4, column l%32.
 #include "hh_kernels.h"
@@ -22,20 +25,15 @@ constexpr int kFlashMaxPages = 2048;  // pages of keys per prefill attention (32
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// The next key blocks' K fragments and V slices are loaded into further
-// register sets while the current block is processed (sets in strict
-// rotation, loads issued unconditionally with clamped keys, so the compiler
-// waits for exactly the oldest set), and V^T is double-buffered in LDS so each
-// block needs a single barrier.
 struct KvRegs {
   f16x8 k, v;  // key idx / 8 of the block, dims (idx % 8) * 8 .. + 8, for this thread's idx
 };
 
 // pt: the stream's page-table slice in LDS (a global read here would make
-// every prefetch wait, in order, for all loads before it).
+// every prefetch wait, in order, for all loads before it).  idx: the thread's
+// index within its group (0 .. 255 stage a block).
 __device__ __forceinline__ void flash_load(KvRegs& R, const _Float16* __restrict__ kv, const KvLayout& L, int layer,
-                                           const int* pt, int g, int k0, int kend) {
-  const int idx = threadIdx.x & 255;
+                                           const int* pt, int g, int idx, int k0, int kend) {
   const int key = min(k0 + (idx >> 3), kend - 1), dc = idx & 7;
   const size_t off = (size_t)(key & 15) * 64 + dc * 8;
   const int page = pt[key >> 4];
@@ -43,21 +41,37 @@ __device__ __forceinline__ void flash_load(KvRegs& R, const _Float16* __restrict
   R.v = *reinterpret_cast<const f16x8*>(kv + L.head_tile(layer, page, 1, g) + off);
 }
 
-template <int G>
-__global__ __launch_bounds__(64 * G) void k_flash_prefill(const _Float16* __restrict__ qM, const _Float16* __restrict__ kv,
-                                                          KvLayout L, int layer, const int* __restrict__ page_table,
-                                                          int s, int p0, int n_rows, int hq, _Float16* __restrict__ oM) {
-  static_assert(G >= 4, "the V slice of a key block needs 256 threads");
-  constexpr int VT_LD = 32 + 8;  // padded row of V^T (halfs)
-  constexpr int KT_LD = 64 + 8;  // padded row of K (halfs)
-  __shared__ __attribute__((aligned(16))) _Float16 vt[2][64 * VT_LD];
-  __shared__ __attribute__((aligned(16))) _Float16 kt[2][32 * KT_LD];
-  __shared__ int pt[kFlashMaxPages];  // physical pages of keys 0 .. kend-1
+template <int G, int NS>
+struct FlashCfg {
+  static constexpr int THREADS = 64 * G * NS;
+  static constexpr int VT_LD = 32 + 8;                 // padded row of V^T (halfs)
+  static constexpr int KT_LD = 64 + 8;                 // padded row of K (halfs)
+  static constexpr int BUF = (64 * VT_LD + 32 * KT_LD) * 2;  // one staged key block, bytes
+  static constexpr int STAGE = NS * 2 * BUF;           // double-buffered, per group
+  // Merge area: groups 1 .. NS-1 leave m, l (64 lanes) and o (32 values x 64 lanes) per wave.
+  static constexpr int MERGE = (NS - 1) * G * (2 + 32) * 64 * 4;
+  static constexpr int PT = kFlashMaxPages * 4;
+  static constexpr int LDS = (STAGE > MERGE ? STAGE : MERGE) + PT;
+  static_assert(G * 64 >= 256, "a group stages a key block with 256 threads");
+  static_assert(THREADS <= 1024, "workgroup size");
+  static_assert(LDS <= 160 * 1024, "LDS");
+};
+
+template <int G, int NS>
+__global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* __restrict__ qM,
+                                                               const _Float16* __restrict__ kv, KvLayout L, int layer,
+                                                               const int* __restrict__ page_table, int s, int p0,
+                                                               int n_rows, int hq, _Float16* __restrict__ oM) {
+  using C = FlashCfg<G, NS>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  int* pt = reinterpret_cast<int*>(smem + (C::LDS - C::PT));  // physical pages of keys 0 .. kend-1
   const int g = blockIdx.y;
   const int qb = gridDim.x - 1 - blockIdx.x;  // longest (latest) query blocks first
   const int q0 = qb * 32;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int j = g * G + wave;
+  const int hi = wave % G, grp = wave / G;
+  const int idx = threadIdx.x - grp * 64 * G;  // thread index within the group
+  const int j = g * G + hi;
   const int h = lane >> 5, c = lane & 31;
   const int qrow = q0 + c;
   const bool qvalid = qrow < n_rows;
@@ -79,33 +93,40 @@ __global__ __launch_bounds__(64 * G) void k_flash_prefill(const _Float16* __rest
   }
   const int kend = min(p0 + q0 + 32, p0 + n_rows);  // keys 0 .. kend-1 exist for this block
   const int nkb = (kend + 31) / 32;
+  const int niter = (nkb + NS - 1) / NS;            // the same for every group (uniform barriers)
   {
     const int* src = page_table + (size_t)s * L.max_pages;
     for (int i = threadIdx.x; i < (kend + kPage - 1) / kPage; i += blockDim.x) pt[i] = src[i];
     __syncthreads();
   }
 
-  auto process = [&](const KvRegs& R, int kb) {
+  char* gbase = smem + grp * 2 * C::BUF;
+  auto process = [&](const KvRegs& R, int it) {
+    const int kb = it * NS + grp;
     const int k0 = kb * 32;
-    _Float16* vb = vt[kb & 1];
-    _Float16* kbuf = kt[kb & 1];
-    // Stage K and V^T of this key block once for all waves (threads 0..255:
-    // key idx / 8, dims (idx % 8) * 8 .. + 8).
-    if (threadIdx.x < 256) {
-      const int key = threadIdx.x >> 3, dc = threadIdx.x & 7;
+    const bool have = kb < nkb;
+    _Float16* vb = reinterpret_cast<_Float16*>(gbase + (it & 1) * C::BUF);
+    _Float16* kbuf = vb + 64 * C::VT_LD;
+    // Stage K and V^T of this key block once for the group's waves (group
+    // threads 0..255: key idx / 8, dims (idx % 8) * 8 .. + 8).
+    if (have && idx < 256) {
+      const int key = idx >> 3, dc = idx & 7;
       const bool ok = k0 + key < kend;
-      *reinterpret_cast<f16x8*>(kbuf + key * KT_LD + dc * 8) = R.k;
+      *reinterpret_cast<f16x8*>(kbuf + key * C::KT_LD + dc * 8) = R.k;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) vb[(dc * 8 + e) * VT_LD + key] = ok ? R.v[e] : (_Float16)0.f;
+      for (int e = 0; e < 8; ++e) vb[(dc * 8 + e) * C::VT_LD + key] = ok ? R.v[e] : (_Float16)0.f;
     }
+    // Buffers alternate, so one barrier per iteration orders this write
+    // after every read of the same buffer two iterations ago.
     __syncthreads();
+    if (!have) return;
 
     f32x16 sacc;
 #pragma unroll
     for (int i = 0; i < 16; ++i) sacc[i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const f16x8 kf = *reinterpret_cast<const f16x8*>(kbuf + c * KT_LD + 16 * ks + 8 * h);
+      const f16x8 kf = *reinterpret_cast<const f16x8*>(kbuf + c * C::KT_LD + 16 * ks + 8 * h);
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[ks], sacc, 0, 0, 0);
     }
 
@@ -119,13 +140,16 @@ __global__ __launch_bounds__(64 * G) void k_flash_prefill(const _Float16* __rest
       bm = fmaxf(bm, v);
     }
     bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-    const float mn = fmaxf(m, bm);  // finite: key 0 of block 0 is visible to every query
-    const float alpha = exp2f(m - mn);
+    // A group's first blocks may hide every key from some query of an
+    // appended chunk: keep such a query's state at (-inf, 0, 0).
+    const float mn = fmaxf(m, bm);
+    const float mref = mn == -INFINITY ? 0.f : mn;
+    const float alpha = exp2f(m - mref);
     float ls = 0.f;
     f16x8 pb[2];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float pv = exp2f(sacc[i] - mn);
+      const float pv = exp2f(sacc[i] - mref);
       ls += pv;
       pb[i >> 3][i & 7] = (_Float16)pv;
     }
@@ -139,8 +163,8 @@ __global__ __launch_bounds__(64 * G) void k_flash_prefill(const _Float16* __rest
     for (int t2 = 0; t2 < 2; ++t2) {
       // A operand: V^T[dim][keys 16 t2 + 4 h + {0..3, 8..11}] for dims c and c + 32.
       f16x8 a0, a1;
-      const _Float16* r0 = vb + c * VT_LD + 16 * t2 + 4 * h;
-      const _Float16* r1 = vb + (c + 32) * VT_LD + 16 * t2 + 4 * h;
+      const _Float16* r0 = vb + c * C::VT_LD + 16 * t2 + 4 * h;
+      const _Float16* r1 = vb + (c + 32) * C::VT_LD + 16 * t2 + 4 * h;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         a0[e] = r0[e];
@@ -154,24 +178,61 @@ __global__ __launch_bounds__(64 * G) void k_flash_prefill(const _Float16* __rest
     m = mn;
   };
 
-  // Three register sets in rotation: blocks kb + 1 and kb + 2 are in flight
-  // while block kb is processed.
-  KvRegs A, B, C;
-  flash_load(A, kv, L, layer, pt, g, 0, kend);
-  flash_load(B, kv, L, layer, pt, g, min(1, nkb - 1) * 32, kend);
-  for (int kb = 0; kb < nkb; kb += 3) {
-    flash_load(C, kv, L, layer, pt, g, min(kb + 2, nkb - 1) * 32, kend);
-    process(A, kb);
-    if (kb + 1 >= nkb) break;
-    flash_load(A, kv, L, layer, pt, g, min(kb + 3, nkb - 1) * 32, kend);
-    process(B, kb + 1);
-    if (kb + 2 >= nkb) break;
-    flash_load(B, kv, L, layer, pt, g, min(kb + 4, nkb - 1) * 32, kend);
-    process(C, kb + 2);
+  // Two register sets in rotation: block it + 1 is in flight while block it
+  // is processed (loads of absent blocks are clamped, never used).
+  KvRegs A, B;
+  const int kcl = (nkb - 1) * 32;
+  if (idx < 256) flash_load(A, kv, L, layer, pt, g, idx, min(grp * 32, kcl), kend);
+  for (int it = 0; it < niter; it += 2) {
+    if (idx < 256) flash_load(B, kv, L, layer, pt, g, idx, min(((it + 1) * NS + grp) * 32, kcl), kend);
+    process(A, it);
+    if (it + 1 >= niter) break;
+    if (idx < 256) flash_load(A, kv, L, layer, pt, g, idx, min(((it + 2) * NS + grp) * 32, kcl), kend);
+    process(B, it + 1);
   }
-  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  lsum += __shfl_xor(lsum, 32, 64);
+
+  // Merge the groups in split order (group 0 holds key block 0, so its max is
+  // finite for every query).
+  if constexpr (NS > 1) {
+    float* mg = reinterpret_cast<float*>(smem);
+    __syncthreads();  // every group is done with its staging buffers
+    if (grp > 0) {
+      float* r = mg + ((grp - 1) * G + hi) * (2 + 32) * 64;
+      r[lane] = m;
+      r[64 + lane] = lsum;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        r[(2 + i) * 64 + lane] = o0[i];
+        r[(18 + i) * 64 + lane] = o1[i];
+      }
+    }
+    __syncthreads();
+    if (grp > 0) return;
+    float mx = m;
+#pragma unroll
+    for (int sp = 1; sp < NS; ++sp) mx = fmaxf(mx, mg[((sp - 1) * G + hi) * (2 + 32) * 64 + lane]);
+    const float w0 = exp2f(m - mx);
+    lsum *= w0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      o0[i] *= w0;
+      o1[i] *= w0;
+    }
+#pragma unroll
+    for (int sp = 1; sp < NS; ++sp) {
+      const float* r = mg + ((sp - 1) * G + hi) * (2 + 32) * 64;
+      const float w = exp2f(r[lane] - mx);  // 0 for a split that saw no key
+      lsum += w * r[64 + lane];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        o0[i] += w * r[(2 + i) * 64 + lane];
+        o1[i] += w * r[(18 + i) * 64 + lane];
+      }
+    }
+  }
   if (qvalid) {
-    const float inv = 1.f / ltot;
+    const float inv = 1.f / lsum;
     _Float16* dst = oM + ((size_t)qrow * hq + j) * 64;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -186,13 +247,26 @@ bool flash_prefill_supported(int G, int max_context) {
   return (G == 4 || G == 8) && (max_context + kPage - 1) / kPage <= kFlashMaxPages;
 }
 
+template <int G, int NS>
+static void launch_flash(hipStream_t st, dim3 grid, const _Float16* qM, const _Float16* kv, KvLayout L, int layer,
+                         const int* page_table, int s, int p0, int n_rows, int hq, _Float16* oM) {
+  using C = FlashCfg<G, NS>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_flash_prefill<G, NS>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    attr = true;
+  }
+  k_flash_prefill<G, NS><<<grid, C::THREADS, C::LDS, st>>>(qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM);
+}
+
 void flash_prefill(hipStream_t st, const _Float16* qM, const _Float16* kv, KvLayout L, int layer,
                    const int* page_table, int s, int p0, int n_rows, int hq, int hkv, _Float16* oM) {
   const int G = hq / hkv;
   dim3 grid((n_rows + 31) / 32, hkv);
   switch (G) {
-    case 4: k_flash_prefill<4><<<grid, 256, 0, st>>>(qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM); break;
-    default: k_flash_prefill<8><<<grid, 512, 0, st>>>(qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM); break;
+    case 4: launch_flash<4, 4>(st, grid, qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM); break;
+    default: launch_flash<8, 2>(st, grid, qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM); break;
   }
 }
 

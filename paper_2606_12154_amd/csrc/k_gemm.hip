@@ -11,8 +11,13 @@
 #include "hh_kernels.h"
 
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <type_traits>
 
 namespace hh {
+
+enum class GemmKind { QKV = 0, Resid = 1, GateUp = 2, Logits = 3 };
 
 // ---------------------------------------------------------------- epilogues
 //
@@ -37,36 +42,46 @@ struct EpiQKV {
   int layer;
   const int* page_table;
   __device__ int b_row(int n) const { return n < (hq + 2 * hkv) * 64 ? n : -1; }
+  // Rotary pair (i, i + 32) of head `head` in row `row`, unscaled.
+  __device__ void head_pair(int row, int head, int i, float y0, float y1) const {
+    y0 *= scale;
+    y1 *= scale;
+    const int s = row_stream[row], p = row_pos[row];
+    if (head < hq + hkv) {
+      const float2 cs = rope[(size_t)p * 32 + i];
+      const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+      if (head < hq) {
+        q[((size_t)row * hq + head) * 64 + i] = r0;
+        q[((size_t)row * hq + head) * 64 + i + 32] = r1;
+        if (qM) {
+          qM[((size_t)row * hq + head) * 64 + i] = (TKV)r0;
+          qM[((size_t)row * hq + head) * 64 + i + 32] = (TKV)r1;
+        }
+      } else {
+        const int page = page_table[(size_t)s * L.max_pages + p / kPage];
+        TKV* dst = kv + L.head_tile(layer, page, 0, head - hq) + (p % kPage) * 64;
+        dst[i] = (TKV)r0;
+        dst[i + 32] = (TKV)r1;
+      }
+    } else {
+      const int page = page_table[(size_t)s * L.max_pages + p / kPage];
+      TKV* dst = kv + L.head_tile(layer, page, 1, head - hq - hkv) + (p % kPage) * 64;
+      dst[i] = (TKV)y0;
+      dst[i + 32] = (TKV)y1;
+    }
+  }
+  // Register epilogue: logical columns cb + c and cb + 32 + c (cb % 64 == 0).
+  __device__ void pair(int row, int cb, int c, float v0, float v1) const {
+    const int head = cb / 64;
+    if (head < hq + 2 * hkv) head_pair(row, head, c, v0, v1);
+  }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     const int nh = BN / 64;
     for (int idx = threadIdx.x; idx < BM * 32 * nh; idx += blockDim.x) {
       const int r = idx / (32 * nh), hh = (idx / 32) % nh, i = idx & 31, row = m0 + r;
       const int head = n0 / 64 + hh;
       if (row >= M || head >= hq + 2 * hkv) continue;
-      const float y0 = Cs[r * ldc + hh * 64 + i] * scale, y1 = Cs[r * ldc + hh * 64 + i + 32] * scale;
-      const int s = row_stream[row], p = row_pos[row];
-      if (head < hq + hkv) {
-        const float2 cs = rope[(size_t)p * 32 + i];
-        const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
-        if (head < hq) {
-          q[((size_t)row * hq + head) * 64 + i] = r0;
-          q[((size_t)row * hq + head) * 64 + i + 32] = r1;
-          if (qM) {
-            qM[((size_t)row * hq + head) * 64 + i] = (TKV)r0;
-            qM[((size_t)row * hq + head) * 64 + i + 32] = (TKV)r1;
-          }
-        } else {
-          const int page = page_table[(size_t)s * L.max_pages + p / kPage];
-          TKV* dst = kv + L.head_tile(layer, page, 0, head - hq) + (p % kPage) * 64;
-          dst[i] = (TKV)r0;
-          dst[i + 32] = (TKV)r1;
-        }
-      } else {
-        const int page = page_table[(size_t)s * L.max_pages + p / kPage];
-        TKV* dst = kv + L.head_tile(layer, page, 1, head - hq - hkv) + (p % kPage) * 64;
-        dst[i] = (TKV)y0;
-        dst[i + 32] = (TKV)y1;
-      }
+      head_pair(row, head, i, Cs[r * ldc + hh * 64 + i], Cs[r * ldc + hh * 64 + i + 32]);
     }
   }
 };
@@ -77,6 +92,11 @@ struct EpiResid {
   float scale;
   float* x;
   __device__ int b_row(int n) const { return n < N ? n : -1; }
+  __device__ void pair(int row, int cb, int c, float v0, float v1) const {
+    float* xr = x + (size_t)row * N + cb + c;
+    if (cb + c < N) xr[0] += v0 * scale;
+    if (cb + 32 + c < N) xr[32] += v1 * scale;
+  }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     for (int idx = threadIdx.x; idx < BM * BN; idx += blockDim.x) {
       const int r = idx / BN, c = idx % BN, row = m0 + r, col = n0 + c;
@@ -85,8 +105,8 @@ struct EpiResid {
   }
 };
 
-// A tile of width BN holds gate columns j = tile * BN/2 + c (c < BN/2) and,
-// in its second half, the matching up columns (rows F + j of [Wg; Wu]);
+// Logical columns come in groups of 2 * half: gate columns j = group * half + c
+// (c < half), then the matching up columns (rows F + j of [Wg; Wu]);
 // m[row, j] = silu(gate) * up.
 template <typename TM>
 struct EpiGateUp {
@@ -97,12 +117,18 @@ struct EpiGateUp {
     const int c = n % (2 * half), j = (n / (2 * half)) * half + (c < half ? c : c - half);
     return j < F ? (c < half ? j : F + j) : -1;
   }
+  // Register epilogue (half == 32): gate column cb + c, up column cb + 32 + c.
+  __device__ void pair(int row, int cb, int c, float v0, float v1) const {
+    const int col = (cb / 64) * 32 + c;
+    if (col < F) m[(size_t)row * F + col] = (TM)(silu(v0 * scale) * (v1 * scale));
+  }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
-    const int j0 = (n0 / BN) * half;
-    for (int idx = threadIdx.x; idx < BM * half; idx += blockDim.x) {
-      const int r = idx / half, c = idx % half, row = m0 + r, col = j0 + c;
+    const int j0 = (n0 / (2 * half)) * half, nc = BN / 2;
+    for (int idx = threadIdx.x; idx < BM * nc; idx += blockDim.x) {
+      const int r = idx / nc, c = idx % nc, row = m0 + r, col = j0 + c;
       if (row >= M || col >= F) continue;
-      const float g = Cs[r * ldc + c] * scale, u = Cs[r * ldc + half + c] * scale;
+      const int cg = (c / half) * 2 * half + c % half;  // gate column in the tile; up is half later
+      const float g = Cs[r * ldc + cg] * scale, u = Cs[r * ldc + cg + half] * scale;
       m[(size_t)row * F + col] = (TM)(silu(g) * u);
     }
   }
@@ -255,6 +281,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // Workgroup barrier without the memory fence __syncthreads() adds (waits are
 // explicit in the caller).
 __device__ __forceinline__ void bare_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// One 16-byte direct global -> LDS load per lane (wave-uniform LDS base).
+// Kept in a device function: the builtin written directly in a kernel body
+// makes the host pass drop the kernel's launch stub without a diagnostic.
+__device__ __forceinline__ void load_lds16(const _Float16* src, char* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
 
 template <int NI, int NW>
 __device__ __forceinline__ void issue_stage(const _Float16* const* src, int koff, char* dst, int wave) {
@@ -420,6 +453,154 @@ __global__ __launch_bounds__(256) void k_splitk_finalize(const float* __restrict
   epi(Cs, LDC, m0, M, n0, kFinRows, BN);
 }
 
+// ---------------------------------------------------------------- wide-tile fp16 kernel (prompt prefill)
+
+// Prompt-sized GEMMs (M >= 256): BM x BN x 64 tiles, one 256-thread workgroup
+// per CU, four waves in a 2 x 2 grid each owning a (BM/2) x (BN/2) block of
+// 32x32x16 MFMAs.  A wave's LDS traffic per MFMA falls with the size of its
+// block (a 128 x 128 block reads 8 KiB of fragments per 16 MFMAs, a 64 x 64
+// block 4 KiB per 4), so large wave blocks keep the LDS well below its
+// bandwidth.  Staging is the same as k_gemm_f16's (whole-line direct loads,
+// (row/2)-swizzled chunks), one barrier per K step: the loads of a step are
+// issued right after the barrier that retires the stage they overwrite.  The
+// epilogue runs from the accumulators: column pairs (c, c + 32) of a 64-column
+// group sit in one lane (blocks 2g and 2g + 1 of the wave), which is the pairing
+// every register epilogue needs (rotary halves, gate / up).
+template <int BM, int BN>
+struct WideTile {
+  static constexpr int BK = 64, NW = 4, THREADS = 256;
+  static constexpr int WM = BM / 2, WN = BN / 2;     // wave block
+  static constexpr int FM = WM / 32, FN = WN / 32;   // 32x32 MFMA blocks per wave
+  static constexpr int GROUPS = (BM + BN) / 8;       // 1 KiB row groups per stage
+  static constexpr int NI = GROUPS / NW;             // load instructions per wave per stage
+  static constexpr int STAGE = GROUPS * 1024;
+  static constexpr int NSTAGE = (160 * 1024) / STAGE >= 3 ? 3 : 2;
+  static constexpr int LDS = NSTAGE * STAGE;
+  static_assert(FN % 2 == 0, "a wave block holds whole 64-column groups");
+  static_assert(GROUPS % NW == 0, "row groups split evenly over the waves");
+  static_assert(NSTAGE * STAGE <= 160 * 1024, "stages fit the LDS");
+  static_assert((NSTAGE - 1) * NI <= 63, "in-flight loads fit the vmcnt range");
+};
+
+template <int BM, int BN, class Epi>
+__global__ __launch_bounds__(256, 1) void k_gemm_wide(const _Float16* __restrict__ A, int M,
+                                                      const _Float16* __restrict__ W, int K, int ntn, int ntiles,
+                                                      int steps_per_split, float* __restrict__ partial, int ncols,
+                                                      Epi epi) {
+  using T = WideTile<BM, BN>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int tile = blockIdx.x % ntiles, split = blockIdx.x / ntiles;
+  const int tn = tile % ntn, tm = tile / ntn;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int nk_all = K / T::BK;
+  const int s0 = split * steps_per_split;
+  const int nk = min(nk_all, s0 + steps_per_split) - s0;
+
+  // Instruction q of wave w fills row group g = w + 4q (stage rows 8g .. 8g + 7):
+  // lane l takes row 8g + l/8, k chunk (l%8) ^ swz(row), swz(r) = (r/2) % 8.
+  const _Float16* src[T::NI];
+#pragma unroll
+  for (int q = 0; q < T::NI; ++q) {
+    const int rr = 8 * (wave + T::NW * q) + (lane >> 3);
+    const int chunk = (lane & 7) ^ ((rr >> 1) & 7);
+    if (rr < BM) {
+      const int row = min(m0 + rr, M - 1);  // rows past M: computed, never stored
+      src[q] = A + (size_t)row * K + (size_t)s0 * T::BK + chunk * 8;
+    } else {
+      const int br = epi.b_row(n0 + rr - BM);
+      src[q] = W + (size_t)(br < 0 ? 0 : br) * K + (size_t)s0 * T::BK + chunk * 8;
+    }
+  }
+
+  f32x16 acc[T::FM][T::FN];
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // Loads are issued unconditionally (K steps past the end re-read the last
+  // one into a stage nobody reads again), so exactly NSTAGE - 2 stages are in
+  // flight behind the current one at every wait, and the scheduling groups
+  // below see one basic block per step.
+  constexpr int kWaitLds = 0xF | (0x7 << 4) | (0x3 << 14);  // lgkmcnt(0)
+#pragma unroll
+  for (int i = 0; i < T::NSTAGE - 1; ++i)
+    issue_stage<T::NI, T::NW>(src, min(i, nk - 1) * T::BK, smem + i * T::STAGE, wave);
+  for (int step = 0; step < nk; ++step) {
+    wait_stages<T::NI>(T::NSTAGE - 2);  // this wave's loads of `step` have landed
+    __builtin_amdgcn_s_waitcnt(kWaitLds);
+    bare_barrier();                     // every wave's have, and every wave is done with step - 1
+    const int ahead = step + T::NSTAGE - 1;
+    const char* sb = smem + (step % T::NSTAGE) * T::STAGE;
+    char* nb = smem + (ahead % T::NSTAGE) * T::STAGE;
+    const int koff = min(ahead, nk - 1) * T::BK;
+    auto frag = [&](int r0, int kb) {
+      const int r = r0 + (lane & 31), c = 2 * kb + (lane >> 5);
+      return *reinterpret_cast<const f16x8*>(sb + r * 128 + 16 * (c ^ ((r >> 1) & 7)));
+    };
+    // Fragments of k block kb + 1 are read while the MFMAs of kb run; the
+    // next stage's global loads are spread over the step's MFMAs.
+    f16x8 a[2][T::FM], b[2][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) a[0][i] = frag(wm * T::WM + i * 32, 0);
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j) b[0][j] = frag(BM + wn * T::WN + j * 32, 0);
+    constexpr int kLoadsPerKb = (T::NI + 3) / 4;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int cur = kb & 1, nxt = cur ^ 1;
+      if (kb < 3) {
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i) a[nxt][i] = frag(wm * T::WM + i * 32, kb + 1);
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) b[nxt][j] = frag(BM + wn * T::WN + j * 32, kb + 1);
+      }
+#pragma unroll
+      for (int q = kb * kLoadsPerKb; q < (kb + 1) * kLoadsPerKb && q < T::NI; ++q)
+        load_lds16(src[q] + koff, nb + (wave + T::NW * q) * 1024);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
+      // Keep the reads and loads of this block ahead of its MFMAs (the
+      // scheduler would otherwise sink each read to just before its first use).
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  wait_stages<T::NI>(0);  // no direct-to-LDS load outlives the workgroup
+  // Element e of lane l in a 32x32 block: row 8(e/4) + 4(l/32) + e%4, column l%32.
+  const int rbase = m0 + wm * T::WM + 4 * (lane >> 5), c = lane & 31;
+  if (partial) {
+    float* dst = partial + (size_t)split * M * ncols;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+          const int col = n0 + wn * T::WN + j * 32 + c;
+          if (r < M && col < ncols) dst[(size_t)r * ncols + col] = acc[i][j][e];
+        }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+    for (int g = 0; g < T::FN / 2; ++g)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+        if (r < M) epi.pair(r, n0 + wn * T::WN + 64 * g, c, acc[i][2 * g][e], acc[i][2 * g + 1][e]);
+      }
+}
+
 // ---------------------------------------------------------------- launchers
 
 template <int BM, class Epi>
@@ -447,13 +628,82 @@ static void launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
     k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn, 256, 0, st>>>(part, splits, M, n_cols, ntn, e);
 }
 
+template <int BM, int BN, class Epi>
+static void launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
+                        int splits, const Epi& e) {
+  using T = WideTile<BM, BN>;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_wide<BM, BN, Epi>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS);
+    attr = true;
+  }
+  const int ntn = (n_cols + BN - 1) / BN;
+  const int ntiles = ((M + BM - 1) / BM) * ntn;
+  const int nk = K / T::BK;
+  splits = std::max(1, std::min(splits, nk / 4));
+  while (splits > 1 && (size_t)splits * M * n_cols * sizeof(float) > ws.bytes) --splits;
+  const int per = (nk + splits - 1) / splits;
+  splits = (nk + per - 1) / per;
+  float* part = splits > 1 ? ws.ptr : nullptr;
+  k_gemm_wide<BM, BN, Epi><<<ntiles * splits, T::THREADS, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
+  if (splits > 1)
+    k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn * (BN / 128), 256, 0, st>>>(part, splits, M, n_cols,
+                                                                                             ntn * (BN / 128), e);
+}
+
+// Tile choice of a prompt-sized GEMM: {BM, BN, splits}, BM == 0 for the
+// small-tile kernel.  HH_GEMM_QKV / _RESID (O projection) / _DOWN / _GATEUP =
+// "BMxBNxS" (or "0") overrides it, for tuning.
+struct WideCfg {
+  int bm, bn, splits;
+};
+
+static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
+  static const char* names[4] = {"HH_GEMM_QKV", "HH_GEMM_RESID", "HH_GEMM_GATEUP", "HH_GEMM_LOGITS"};
+  // The down projection (K > N) has a knob of its own.
+  const char* env = getenv(kind == GemmKind::Resid && K > n_cols ? "HH_GEMM_DOWN" : names[(int)kind]);
+  if (env) {
+    WideCfg c{0, 0, 1};
+    if (sscanf(env, "%dx%dx%d", &c.bm, &c.bn, &c.splits) >= 2) return c;
+    return WideCfg{0, 0, 1};
+  }
+  // Measured on the 1B prompt shapes (d 2048, FFN 8192): gate/up at 1024 rows
+  // 88.9 -> ~72 us with 256 x 256 tiles (256 tiles, one per CU); the down
+  // projection (K 8192, only 128 tiles of 128 x 128) gains most from a 2-way
+  // K split; QKV and O, and everything at 256 rows, stay on the small-tile
+  // kernel, whose two workgroups per CU suit these few-tile shapes better.
+  if (kind == GemmKind::GateUp && n_cols >= 8192) {
+    if (M >= 512) return WideCfg{256, 256, 1};
+    if (M >= 256) return WideCfg{128, 128, 1};
+  }
+  if (kind == GemmKind::Resid && K > n_cols && M >= 512) return WideCfg{128, 128, 2};
+  return WideCfg{0, 0, 1};
+}
+
+template <class Epi>
+static bool run_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
+                     const Epi& e, GemmKind kind) {
+  if (kind == GemmKind::Logits || M < 128) return false;
+  const WideCfg c = wide_choice(kind, M, n_cols, K);
+  if (c.bm == 256 && c.bn == 256) launch_wide<256, 256>(st, ws, A, M, W, K, n_cols, c.splits, e);
+  else if (c.bm == 256 && c.bn == 128) launch_wide<256, 128>(st, ws, A, M, W, K, n_cols, c.splits, e);
+  else if (c.bm == 128 && c.bn == 256) launch_wide<128, 256>(st, ws, A, M, W, K, n_cols, c.splits, e);
+  else if (c.bm == 128 && c.bn == 128) launch_wide<128, 128>(st, ws, A, M, W, K, n_cols, c.splits, e);
+  else return false;
+  return true;
+}
+
 // Run C = A W^T over n_cols logical columns with epilogue e.
 template <typename TM, class Epi>
-static void run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e) {
+static void run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e,
+                     GemmKind kind) {
   if constexpr (sizeof(TM) == 2) {
     if (K % 64 == 0) {
       const _Float16* Ah = reinterpret_cast<const _Float16*>(A);
       const _Float16* Wh = reinterpret_cast<const _Float16*>(W);
+      if constexpr (!std::is_same<Epi, EpiLogits>::value)
+        if (run_wide(st, ws, Ah, M, Wh, K, n_cols, e, kind)) return;
       const long long ntn = (n_cols + 127) / 128;
       if (M <= 32) launch_f16<32>(st, ws, Ah, M, Wh, K, n_cols, e);
       else if (M <= 64 || ((M + 127) / 128) * ntn < 256) launch_f16<64>(st, ws, Ah, M, Wh, K, n_cols, e);
@@ -469,30 +719,29 @@ void GemmKernels<TM, TKV>::qkv(hipStream_t st, GemmWorkspace ws, const TM* A, in
                                const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM,
                                TKV* kv, KvLayout L, int layer, const int* page_table) {
   EpiQKV<TKV> e{hq, hkv, scale, row_stream, row_pos, rope, q, reinterpret_cast<TKV*>(qM), kv, L, layer, page_table};
-  run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e);
+  run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e, GemmKind::QKV);
 }
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale,
                                  float* x) {
   EpiResid e{N, scale, x};
-  run_gemm<TM>(st, ws, A, M, W, K, N, e);
+  run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid);
 }
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale,
                                   TM* m) {
-  // Tile width: 128 on the fp16 path, 64 on the generic one; half of it gate.
-  const int bn = (sizeof(TM) == 2 && d % 64 == 0) ? 128 : GBN;
-  EpiGateUp<TM> e{F, bn / 2, scale, m};
-  run_gemm<TM>(st, ws, A, M, W, d, ((F + bn / 2 - 1) / (bn / 2)) * bn, e);
+  // Groups of 32 gate + 32 up columns: every tile width here is a multiple of 64.
+  EpiGateUp<TM> e{F, 32, scale, m};
+  run_gemm<TM>(st, ws, A, M, W, d, ((F + 31) / 32) * 64, e, GemmKind::GateUp);
 }
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale,
                                   float* logits, unsigned long long* slot, const int* row_stream) {
   EpiLogits e{V, scale, logits, slot, row_stream};
-  run_gemm<TM>(st, ws, A, M, W, d, V, e);
+  run_gemm<TM>(st, ws, A, M, W, d, V, e, GemmKind::Logits);
 }
 
 template struct GemmKernels<float, float>;

@@ -4,6 +4,8 @@ oracle over the whole vocabulary, argmax equal wherever the oracle's top-2
 margin exceeds 1e-2.  The oracle consumes the same bf16 weights widened to
 fp64; the GPU keeps the KV cache in fp16 and feeds its MFMA path fp16
 operands, the only sources of difference beyond summation order."""
+import os
+
 import numpy as np
 import pytest
 
@@ -31,14 +33,62 @@ def ctx(one_b):
     c.close()
 
 
-def test_prefill_256_all_logits(one_b, ctx):
+@pytest.fixture(scope="module")
+def prompt_ref(one_b):
+    """Oracle logits of every row of the 256-token prompt (by causality, the
+    first n rows are also the logits of the prompt's first n tokens)."""
     shape, _, model = one_b
     toks = synth.make_tokens(shape.vocab, 256, 2)
     ref, _ = model.prefill(toks)
+    return toks, ref
+
+
+def test_prefill_256_all_logits(one_b, ctx, prompt_ref):
+    toks, ref = prompt_ref
     ctx.reset()
     nxt, got = ctx.prefill(0, toks, logits="all")
     worst = check_logits(got, ref, TOL, what="1B prefill all")
     print(f"1B prefill 256 rows: max-abs {worst:.4g}")
+    assert nxt == int(np.argmax(got[-1]))
+
+
+@pytest.mark.parametrize("cut", [72, 129])
+def test_prefill_appended_chunk(one_b, ctx, prompt_ref, cut):
+    """A prompt fed in two calls: the second chunk's queries start mid key
+    block, so some key-split groups of the flash kernel see no visible key for
+    some queries."""
+    toks, ref = prompt_ref
+    ctx.reset()
+    ctx.prefill(0, toks[:cut])
+    nxt, got = ctx.prefill(0, toks[cut:200], logits="all")
+    worst = check_logits(got, ref[cut:200], TOL, what=f"1B appended chunk {cut}:200")
+    print(f"1B appended chunk {cut}:200: max-abs {worst:.4g}")
+    assert nxt == int(np.argmax(got[-1]))
+
+
+GEMM_KINDS = ("HH_GEMM_QKV", "HH_GEMM_RESID", "HH_GEMM_DOWN", "HH_GEMM_GATEUP")
+
+
+@pytest.mark.parametrize("tile", ["256x256x1", "256x128x1", "128x256x1", "128x128x1", "256x256x4", "128x128x2"])
+@pytest.mark.parametrize("n", [256, 200])
+def test_prefill_wide_tiles(one_b, ctx, prompt_ref, tile, n):
+    """Every large-tile GEMM shape (and split-K) of the prompt path, forced
+    for the QKV, residual and gate/up GEMMs, on a whole and a ragged row count."""
+    toks, ref = prompt_ref
+    saved = {k: os.environ.get(k) for k in GEMM_KINDS}
+    try:
+        for k in GEMM_KINDS:
+            os.environ[k] = tile
+        ctx.reset()
+        nxt, got = ctx.prefill(0, toks[:n], logits="all")
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    worst = check_logits(got, ref[:n], TOL, what=f"1B prefill {n} rows, tiles {tile}")
+    print(f"1B prefill {n} rows, tiles {tile}: max-abs {worst:.4g}")
     assert nxt == int(np.argmax(got[-1]))
 
 
