@@ -44,7 +44,13 @@ struct GemmKernels {
   static void qkv(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
                   const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM, TKV* kv,
                   KvLayout L, int layer, const int* page_table);
-  static void resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x);
+  // x += A W^T * scale; with gain, then h = rmsnorm(x) * gain (fused into the
+  // split-K reduction when K is split).  Requires norm_fusable(N) with gain.
+  static void resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x,
+                    const float* gain = nullptr, float eps = 0.f, TM* h = nullptr);
+  static bool norm_fusable(int N);
+  // h = rmsnorm(x) * gain, one row per workgroup (norm_fusable(N)).
+  static void rmsnorm(hipStream_t st, int M, float* x, int N, const float* gain, float eps, TM* h);
   static void gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale, TM* m);
   static void logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale, float* logits,
                      unsigned long long* slot, const int* row_stream);

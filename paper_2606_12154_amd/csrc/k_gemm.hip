@@ -75,6 +75,8 @@ struct EpiQKV {
     const int head = cb / 64;
     if (head < hq + 2 * hkv) head_pair(row, head, c, v0, v1);
   }
+  // The same for a column group known to be in range.
+  __device__ void pair_full(int row, int cb, int c, float v0, float v1) const { head_pair(row, cb / 64, c, v0, v1); }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     const int nh = BN / 64;
     for (int idx = threadIdx.x; idx < BM * 32 * nh; idx += blockDim.x) {
@@ -96,6 +98,11 @@ struct EpiResid {
     float* xr = x + (size_t)row * N + cb + c;
     if (cb + c < N) xr[0] += v0 * scale;
     if (cb + 32 + c < N) xr[32] += v1 * scale;
+  }
+  __device__ void pair_full(int row, int cb, int c, float v0, float v1) const {
+    float* xr = x + (size_t)row * N + cb + c;
+    xr[0] += v0 * scale;
+    xr[32] += v1 * scale;
   }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     for (int idx = threadIdx.x; idx < BM * BN; idx += blockDim.x) {
@@ -121,6 +128,12 @@ struct EpiGateUp {
   __device__ void pair(int row, int cb, int c, float v0, float v1) const {
     const int col = (cb / 64) * 32 + c;
     if (col < F) m[(size_t)row * F + col] = (TM)(silu(v0 * scale) * (v1 * scale));
+  }
+  // In-range group; SiLU with the hardware reciprocal (the result is rounded
+  // to fp16 right after, far coarser than its 1-ulp error).
+  __device__ void pair_full(int row, int cb, int c, float v0, float v1) const {
+    const float gt = v0 * scale;
+    m[(size_t)row * F + (cb / 64) * 32 + c] = (TM)(gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * (v1 * scale));
   }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     const int j0 = (n0 / (2 * half)) * half, nc = BN / 2;
@@ -590,6 +603,20 @@ __global__ __launch_bounds__(256, 1) void k_gemm_wide(const _Float16* __restrict
         }
     return;
   }
+  if (m0 + BM <= M && n0 + BN <= ncols) {
+    // Whole tile in range (every tile of a prompt whose length is a multiple
+    // of BM): no per-element guards, which would otherwise turn the unrolled
+    // epilogue into thousands of exec-mask branches.
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+      for (int g = 0; g < T::FN / 2; ++g)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          epi.pair_full(rbase + i * 32 + 8 * (e >> 2) + (e & 3), n0 + wn * T::WN + 64 * g, c, acc[i][2 * g][e],
+                        acc[i][2 * g + 1][e]);
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < T::FM; ++i)
 #pragma unroll
@@ -603,8 +630,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_wide(const _Float16* __restrict
 
 // ---------------------------------------------------------------- launchers
 
+// Launchers return the number of K splits used.  With defer set, split
+// partials are left in the workspace for the caller to reduce (1: the
+// epilogue already ran).
 template <int BM, class Epi>
-static void launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols, const Epi& e) {
+static int launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
+                      const Epi& e, bool defer) {
   using T = F16Tile<BM>;
   static bool attr = false;
   if (!attr) {
@@ -624,13 +655,14 @@ static void launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
   splits = (nk + per - 1) / per;
   float* part = splits > 1 ? ws.ptr : nullptr;
   k_gemm_f16<BM, Epi><<<ntiles * splits, T::THREADS, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
-  if (splits > 1)
+  if (splits > 1 && !defer)
     k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn, 256, 0, st>>>(part, splits, M, n_cols, ntn, e);
+  return splits;
 }
 
 template <int BM, int BN, class Epi>
-static void launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
-                        int splits, const Epi& e) {
+static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
+                       int splits, const Epi& e, bool defer) {
   using T = WideTile<BM, BN>;
   static bool attr = false;
   if (!attr) {
@@ -647,9 +679,10 @@ static void launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int
   splits = (nk + per - 1) / per;
   float* part = splits > 1 ? ws.ptr : nullptr;
   k_gemm_wide<BM, BN, Epi><<<ntiles * splits, T::THREADS, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
-  if (splits > 1)
+  if (splits > 1 && !defer)
     k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn * (BN / 128), 256, 0, st>>>(part, splits, M, n_cols,
                                                                                              ntn * (BN / 128), e);
+  return splits;
 }
 
 // Tile choice of a prompt-sized GEMM: {BM, BN, splits}, BM == 0 for the
@@ -670,48 +703,113 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
   }
   // Measured on the 1B prompt shapes (d 2048, FFN 8192): gate/up at 1024 rows
   // 88.9 -> ~72 us with 256 x 256 tiles (256 tiles, one per CU); the down
-  // projection (K 8192, only 128 tiles of 128 x 128) gains most from a 2-way
-  // K split; QKV and O, and everything at 256 rows, stay on the small-tile
-  // kernel, whose two workgroups per CU suit these few-tile shapes better.
+  // and O projections (only 128 tiles of 128 x 128) gain most from a 2-way K
+  // split; QKV, and everything at 256 rows, stay on the small-tile kernel,
+  // whose two workgroups per CU suit these few-tile shapes better.
   if (kind == GemmKind::GateUp && n_cols >= 8192) {
     if (M >= 512) return WideCfg{256, 256, 1};
     if (M >= 256) return WideCfg{128, 128, 1};
   }
-  if (kind == GemmKind::Resid && K > n_cols && M >= 512) return WideCfg{128, 128, 2};
+  if (kind == GemmKind::Resid && M >= 512) return WideCfg{128, 128, 2};
   return WideCfg{0, 0, 1};
 }
 
+// Returns the splits used, 0 when the shape is left to the small-tile kernel.
 template <class Epi>
-static bool run_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
-                     const Epi& e, GemmKind kind) {
-  if (kind == GemmKind::Logits || M < 128) return false;
+static int run_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
+                    const Epi& e, GemmKind kind, bool defer) {
+  if (kind == GemmKind::Logits || M < 128) return 0;
   const WideCfg c = wide_choice(kind, M, n_cols, K);
-  if (c.bm == 256 && c.bn == 256) launch_wide<256, 256>(st, ws, A, M, W, K, n_cols, c.splits, e);
-  else if (c.bm == 256 && c.bn == 128) launch_wide<256, 128>(st, ws, A, M, W, K, n_cols, c.splits, e);
-  else if (c.bm == 128 && c.bn == 256) launch_wide<128, 256>(st, ws, A, M, W, K, n_cols, c.splits, e);
-  else if (c.bm == 128 && c.bn == 128) launch_wide<128, 128>(st, ws, A, M, W, K, n_cols, c.splits, e);
-  else return false;
-  return true;
+  if (c.bm == 256 && c.bn == 256) return launch_wide<256, 256>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+  if (c.bm == 256 && c.bn == 128) return launch_wide<256, 128>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+  if (c.bm == 128 && c.bn == 256) return launch_wide<128, 256>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+  if (c.bm == 128 && c.bn == 128) return launch_wide<128, 128>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+  return 0;
 }
 
-// Run C = A W^T over n_cols logical columns with epilogue e.
+// Run C = A W^T over n_cols logical columns with epilogue e; returns the K
+// splits used (with defer, partials of a split run are left in ws.ptr).
 template <typename TM, class Epi>
-static void run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e,
-                     GemmKind kind) {
+static int run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e,
+                    GemmKind kind, bool defer = false) {
   if constexpr (sizeof(TM) == 2) {
     if (K % 64 == 0) {
       const _Float16* Ah = reinterpret_cast<const _Float16*>(A);
       const _Float16* Wh = reinterpret_cast<const _Float16*>(W);
-      if constexpr (!std::is_same<Epi, EpiLogits>::value)
-        if (run_wide(st, ws, Ah, M, Wh, K, n_cols, e, kind)) return;
+      if constexpr (!std::is_same<Epi, EpiLogits>::value) {
+        const int sp = run_wide(st, ws, Ah, M, Wh, K, n_cols, e, kind, defer);
+        if (sp > 0) return sp;
+      }
       const long long ntn = (n_cols + 127) / 128;
-      if (M <= 32) launch_f16<32>(st, ws, Ah, M, Wh, K, n_cols, e);
-      else if (M <= 64 || ((M + 127) / 128) * ntn < 256) launch_f16<64>(st, ws, Ah, M, Wh, K, n_cols, e);
-      else launch_f16<128>(st, ws, Ah, M, Wh, K, n_cols, e);
-      return;
+      if (M <= 32) return launch_f16<32>(st, ws, Ah, M, Wh, K, n_cols, e, defer);
+      if (M <= 64 || ((M + 127) / 128) * ntn < 256) return launch_f16<64>(st, ws, Ah, M, Wh, K, n_cols, e, defer);
+      return launch_f16<128>(st, ws, Ah, M, Wh, K, n_cols, e, defer);
     }
   }
   k_gemm<TM, Epi><<<dim3((n_cols + GBN - 1) / GBN, (M + GBM - 1) / GBM), 256, 0, st>>>(A, M, W, K, e);
+  return 1;
+}
+
+// ---------------------------------------------------------------- residual + RMSNorm
+
+// One row per workgroup: x[row] += (sum of the split partials, in split
+// order) * scale when splits > 0, then h[row] = x[row] * rsqrt(mean(x^2) +
+// eps) * gain in the MFMA operand type.  The row (N % 4 == 0, N <= 4096) stays
+// in registers between the two halves.
+constexpr int kNormMaxChunks = 4;  // float4 chunks per thread: N <= 4096
+template <typename TM>
+__global__ __launch_bounds__(256) void k_resid_norm(const float* __restrict__ partial, int splits, int M, int N, float scale,
+                                                    float* __restrict__ x, const float* __restrict__ gain, float eps,
+                                                    TM* __restrict__ h) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, nc = N >> 2;
+  float4* xr = reinterpret_cast<float4*>(x + (size_t)row * N);
+  float4 v[kNormMaxChunks];
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < kNormMaxChunks; ++k) {
+    const int ch = threadIdx.x + 256 * k;
+    if (ch < nc) {
+      float4 a = xr[ch];
+      if (splits > 0) {
+        const float4* pp = reinterpret_cast<const float4*>(partial + (size_t)row * N) + ch;
+        const size_t stride = (size_t)M * nc;  // one split's partials, in float4
+        float4 t = pp[0];
+        for (int sp = 1; sp < splits; ++sp) {
+          const float4 u = pp[sp * stride];
+          t.x += u.x;
+          t.y += u.y;
+          t.z += u.z;
+          t.w += u.w;
+        }
+        a.x += t.x * scale;
+        a.y += t.y * scale;
+        a.z += t.z * scale;
+        a.w += t.w * scale;
+        xr[ch] = a;
+      }
+      v[k] = a;
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+    }
+  }
+  const float inv = rsqrtf(block_sum256(ss, red) / (float)N + eps);
+#pragma unroll
+  for (int k = 0; k < kNormMaxChunks; ++k) {
+    const int ch = threadIdx.x + 256 * k;
+    if (ch < nc) {
+      const float4 g = reinterpret_cast<const float4*>(gain)[ch];
+      TM* hr = h + (size_t)row * N + 4 * ch;
+      if constexpr (sizeof(TM) == 2) {
+        typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+        const f16x4 o = {(_Float16)(v[k].x * inv * g.x), (_Float16)(v[k].y * inv * g.y), (_Float16)(v[k].z * inv * g.z),
+                         (_Float16)(v[k].w * inv * g.w)};
+        *reinterpret_cast<f16x4*>(hr) = o;
+      } else {
+        *reinterpret_cast<float4*>(hr) = make_float4(v[k].x * inv * g.x, v[k].y * inv * g.y, v[k].z * inv * g.z,
+                                                     v[k].w * inv * g.w);
+      }
+    }
+  }
 }
 
 template <typename TM, typename TKV>
@@ -723,10 +821,22 @@ void GemmKernels<TM, TKV>::qkv(hipStream_t st, GemmWorkspace ws, const TM* A, in
 }
 
 template <typename TM, typename TKV>
+bool GemmKernels<TM, TKV>::norm_fusable(int N) {
+  return N % 4 == 0 && N <= 4 * 256 * kNormMaxChunks;
+}
+
+template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale,
-                                 float* x) {
+                                 float* x, const float* gain, float eps, TM* h) {
   EpiResid e{N, scale, x};
-  run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid);
+  const bool norm = gain != nullptr;
+  const int sp = run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid, norm);
+  if (norm) k_resid_norm<TM><<<M, 256, 0, st>>>(ws.ptr, sp > 1 ? sp : 0, M, N, scale, x, gain, eps, h);
+}
+
+template <typename TM, typename TKV>
+void GemmKernels<TM, TKV>::rmsnorm(hipStream_t st, int M, float* x, int N, const float* gain, float eps, TM* h) {
+  k_resid_norm<TM><<<M, 256, 0, st>>>(nullptr, 0, M, N, 1.f, x, gain, eps, h);
 }
 
 template <typename TM, typename TKV>

@@ -241,7 +241,11 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       TM* h = c->at<TM>(L.h);
       TM* oM = c->at<TM>(L.oM);
       TM* mM = c->at<TM>(L.mM);
-      DK::rmsnorm_rows(st, n, x, an, eps, d, h);
+      // The attention norm of layer l > 0 was fused into layer l - 1's down
+      // projection (its split-K reduction when K is split).
+      const bool fuse = GK::norm_fusable(d);
+      if (!fuse) DK::rmsnorm_rows(st, n, x, an, eps, d, h);
+      else if (l == 0) GK::rmsnorm(st, n, x, d, an, eps, h);
       // Prefill rows of one stream with an fp16 cache use MFMA flash attention.
       const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv, c->cfg.max_context);
       GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, flash ? c->at<TM>(L.qM) : nullptr,
@@ -255,10 +259,15 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       } else {
         DK::attention_rows(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, o32, oM);
       }
-      GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
-      DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
+      if (fuse) {
+        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h);
+      } else {
+        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
+        DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
+      }
       GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM);
-      GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x);
+      const float* next_an = (fuse && l + 1 < g.n_layers) ? c->at<float>(L.attn_norm[l + 1]) : nullptr;
+      GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h);
     }
   }
   const float* fn = c->at<float>(L.final_norm);
@@ -269,7 +278,8 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       DK::head_gemv(st, c->at<TW>(L.lm_head), x, fn, eps, d, V, 0, rs, logits, slot);
     } else {
       TM* h = c->at<TM>(L.h);
-      DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
+      if (GK::norm_fusable(d)) GK::rmsnorm(st, n, x, d, fn, eps, h);
+      else DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
       GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs);
     }
   }
