@@ -19,6 +19,8 @@ namespace hh {
 
 enum class GemmKind { QKV = 0, Resid = 1, GateUp = 2, Logits = 3 };
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
 // ---------------------------------------------------------------- epilogues
 //
 // The GEMM works on logical columns n; epi.b_row(n) names the weight row of
@@ -51,8 +53,10 @@ struct EpiQKV {
       const float2 cs = rope[(size_t)p * 32 + i];
       const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
       if (head < hq) {
-        q[((size_t)row * hq + head) * 64 + i] = r0;
-        q[((size_t)row * hq + head) * 64 + i + 32] = r1;
+        if (q) {
+          q[((size_t)row * hq + head) * 64 + i] = r0;
+          q[((size_t)row * hq + head) * 64 + i + 32] = r1;
+        }
         if (qM) {
           qM[((size_t)row * hq + head) * 64 + i] = (TKV)r0;
           qM[((size_t)row * hq + head) * 64 + i + 32] = (TKV)r1;
@@ -75,8 +79,54 @@ struct EpiQKV {
     const int head = cb / 64;
     if (head < hq + 2 * hkv) head_pair(row, head, c, v0, v1);
   }
-  // The same for a column group known to be in range.
-  __device__ void pair_full(int row, int cb, int c, float v0, float v1) const { head_pair(row, cb / 64, c, v0, v1); }
+  // A wave's whole in-range 64-column group (one head) for FM x 16 rows:
+  // element e of accumulator block i is row rb + 32 i + 8 (e / 4) + e % 4.
+  // The head's kind is decided once for all its rows.
+  template <int FM>
+  __device__ void group_full(int rb, int cb, int c, const f32x16* a0, const f32x16* a1) const {
+    const int head = cb / 64;
+    if (head < hq) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = rb + 32 * i + 8 * (e >> 2) + (e & 3);
+          const float y0 = a0[i][e] * scale, y1 = a1[i][e] * scale;
+          const float2 cs = rope[(size_t)row_pos[row] * 32 + c];
+          const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+          const size_t o = ((size_t)row * hq + head) * 64 + c;
+          if (q) {
+            q[o] = r0;
+            q[o + 32] = r1;
+          }
+          if (qM) {
+            qM[o] = (TKV)r0;
+            qM[o + 32] = (TKV)r1;
+          }
+        }
+    } else {
+      const bool isk = head < hq + hkv;
+      const int kvh = isk ? head - hq : head - hq - hkv;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = rb + 32 * i + 8 * (e >> 2) + (e & 3);
+          float y0 = a0[i][e] * scale, y1 = a1[i][e] * scale;
+          const int p = row_pos[row];
+          if (isk) {
+            const float2 cs = rope[(size_t)p * 32 + c];
+            const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+            y0 = r0;
+            y1 = r1;
+          }
+          const int page = page_table[(size_t)row_stream[row] * L.max_pages + p / kPage];
+          TKV* dst = kv + L.head_tile(layer, page, isk ? 0 : 1, kvh) + (p % kPage) * 64 + c;
+          dst[0] = (TKV)y0;
+          dst[32] = (TKV)y1;
+        }
+    }
+  }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     const int nh = BN / 64;
     for (int idx = threadIdx.x; idx < BM * 32 * nh; idx += blockDim.x) {
@@ -99,10 +149,16 @@ struct EpiResid {
     if (cb + c < N) xr[0] += v0 * scale;
     if (cb + 32 + c < N) xr[32] += v1 * scale;
   }
-  __device__ void pair_full(int row, int cb, int c, float v0, float v1) const {
-    float* xr = x + (size_t)row * N + cb + c;
-    xr[0] += v0 * scale;
-    xr[32] += v1 * scale;
+  template <int FM>
+  __device__ void group_full(int rb, int cb, int c, const f32x16* a0, const f32x16* a1) const {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float* xr = x + (size_t)(rb + 32 * i + 8 * (e >> 2) + (e & 3)) * N + cb + c;
+        xr[0] += a0[i][e] * scale;
+        xr[32] += a1[i][e] * scale;
+      }
   }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     for (int idx = threadIdx.x; idx < BM * BN; idx += blockDim.x) {
@@ -131,9 +187,17 @@ struct EpiGateUp {
   }
   // In-range group; SiLU with the hardware reciprocal (the result is rounded
   // to fp16 right after, far coarser than its 1-ulp error).
-  __device__ void pair_full(int row, int cb, int c, float v0, float v1) const {
-    const float gt = v0 * scale;
-    m[(size_t)row * F + (cb / 64) * 32 + c] = (TM)(gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * (v1 * scale));
+  template <int FM>
+  __device__ void group_full(int rb, int cb, int c, const f32x16* a0, const f32x16* a1) const {
+    TM* mc = m + (cb / 64) * 32 + c;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float gt = a0[i][e] * scale;
+        mc[(size_t)(rb + 32 * i + 8 * (e >> 2) + (e & 3)) * F] =
+            (TM)(gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * (a1[i][e] * scale));
+      }
   }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
     const int j0 = (n0 / (2 * half)) * half, nc = BN / 2;
@@ -289,7 +353,6 @@ struct F16Tile {
   static_assert(GROUPS % NW == 0, "row groups split evenly over the waves");
 };
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Workgroup barrier without the memory fence __syncthreads() adds (waits are
 // explicit in the caller).
@@ -608,13 +671,15 @@ __global__ __launch_bounds__(256, 1) void k_gemm_wide(const _Float16* __restrict
     // of BM): no per-element guards, which would otherwise turn the unrolled
     // epilogue into thousands of exec-mask branches.
 #pragma unroll
-    for (int i = 0; i < T::FM; ++i)
+    for (int g = 0; g < T::FN / 2; ++g) {
+      f32x16 a0[T::FM], a1[T::FM];
 #pragma unroll
-      for (int g = 0; g < T::FN / 2; ++g)
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          epi.pair_full(rbase + i * 32 + 8 * (e >> 2) + (e & 3), n0 + wn * T::WN + 64 * g, c, acc[i][2 * g][e],
-                        acc[i][2 * g + 1][e]);
+      for (int i = 0; i < T::FM; ++i) {
+        a0[i] = acc[i][2 * g];
+        a1[i] = acc[i][2 * g + 1];
+      }
+      epi.template group_full<T::FM>(rbase, n0 + wn * T::WN + 64 * g, c, a0, a1);
+    }
     return;
   }
 #pragma unroll

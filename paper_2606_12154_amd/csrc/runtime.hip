@@ -248,8 +248,9 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       else if (l == 0) GK::rmsnorm(st, n, x, d, an, eps, h);
       // Prefill rows of one stream with an fp16 cache use MFMA flash attention.
       const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv, c->cfg.max_context);
-      GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, flash ? c->at<TM>(L.qM) : nullptr,
-              kv, kl, l, pt);
+      // Flash attention reads only the fp16 queries.
+      GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, flash ? nullptr : q,
+              flash ? c->at<TM>(L.qM) : nullptr, kv, kl, l, pt);
       if (flash) {
         if constexpr (sizeof(TKV) == 2)
           flash_prefill(st, reinterpret_cast<const _Float16*>(c->at<TM>(L.qM)), reinterpret_cast<const _Float16*>(kv),
