@@ -41,19 +41,22 @@ struct GemmWorkspace {
 
 template <typename TM, typename TKV>
 struct GemmKernels {
+  // Wt (optional): the same matrix as 16 x 32 operand tiles (tile16), used
+  // for M <= 32 rows.
   static void qkv(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
                   const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM, TKV* kv,
-                  KvLayout L, int layer, const int* page_table);
+                  KvLayout L, int layer, const int* page_table, const TM* Wt = nullptr);
   // x += A W^T * scale; with gain, then h = rmsnorm(x) * gain (fused into the
   // split-K reduction when K is split).  Requires norm_fusable(N) with gain.
   static void resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x,
-                    const float* gain = nullptr, float eps = 0.f, TM* h = nullptr);
+                    const float* gain = nullptr, float eps = 0.f, TM* h = nullptr, const TM* Wt = nullptr);
   static bool norm_fusable(int N);
   // h = rmsnorm(x) * gain, one row per workgroup (norm_fusable(N)).
   static void rmsnorm(hipStream_t st, int M, float* x, int N, const float* gain, float eps, TM* h);
-  static void gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale, TM* m);
+  static void gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale, TM* m,
+                     const TM* Wt = nullptr);
   static void logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale, float* logits,
-                     unsigned long long* slot, const int* row_stream);
+                     unsigned long long* slot, const int* row_stream, const TM* Wt = nullptr);
 };
 
 // ---- causal flash attention for prefill rows of one stream (k_attn_prefill.hip)
@@ -135,6 +138,9 @@ struct StepKernel {
 void widen_bf16(hipStream_t st, const __bf16* src, float* dst, size_t n);
 void absmax_bf16(hipStream_t st, const __bf16* src, size_t n, unsigned int* out_bits);
 void bf16_to_f16_scaled(hipStream_t st, const __bf16* src, _Float16* dst, size_t n, float scale);
+// 16 x 32 operand tiles of a [rows][K] fp16 matrix taken as logical_rows rows
+// (see k_tile16); dst holds ceil(logical_rows / 16) * 16 * K elements.
+void tile16(hipStream_t st, const _Float16* src, _Float16* dst, int rows, int K, int logical_rows, int interleave_f);
 // dst = src^T for a row-major rows x cols matrix.
 template <typename T>
 void transpose(hipStream_t st, const T* src, T* dst, int rows, int cols);

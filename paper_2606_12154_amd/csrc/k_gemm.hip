@@ -750,6 +750,153 @@ static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
   return splits;
 }
 
+// ---------------------------------------------------------------- skinny kernel (<= 32 rows)
+
+// Lockstep multi-stream decode: C[M <= 32, N] = A W^T is weight streaming, not
+// arithmetic.  A workgroup owns 64 logical columns (one QKV head, 32 gate + 32
+// up columns, or 64 residual columns) and one K range; its four waves take 16
+// weight rows each.  Weights go from HBM straight into registers as the A
+// operand of 16x16x32 MFMAs (lane l: row l%16, k 8(l/16) .. + 8), in
+// batches of eight K blocks with the next batch loading while one computes;
+// the activations (at most 32 rows) of each batch are loaded once per
+// workgroup, coalesced, into double-buffered LDS (16-byte row padding keeps
+// the B fragment reads conflict-free).  The finished
+// 64-column tile goes through LDS into the usual epilogue, or into split
+// partials when K is split to give every CU work.
+template <class Epi, int U>
+__global__ __launch_bounds__(256) void k_gemm_skinny(const _Float16* __restrict__ A, int M, const _Float16* __restrict__ Wt,
+                                                     int K, int nb, int steps_per_split, float* __restrict__ partial,
+                                                     int ncols, Epi epi) {
+  constexpr int XP = 32 * U + 8;              // LDS row pitch of an activation chunk (halfs; 16 bytes of padding)
+  constexpr int XCH = 32 * (32 * U / 8);      // 16-byte chunks per activation batch (32 rows)
+  static_assert(XCH % 256 == 0, "activation chunks split evenly over the threads");
+  __shared__ __attribute__((aligned(16))) _Float16 xs[2][32 * XP];
+  const int cb = blockIdx.x % nb, split = blockIdx.x / nb;
+  const int n0 = cb * 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int k0 = split * steps_per_split * 32;
+  const int nkb = min(K - k0, steps_per_split * 32) / 32;  // K blocks of 32 in this range
+
+  // Weights (16 x 32 operand tiles, 1 KiB each in lane order, so a load
+  // instruction reads one contiguous KiB) and activations both come through
+  // range-checked buffer loads: the batches need no clamping (blocks past this
+  // range read further on, or zeros past the matrix, and are never used), and
+  // activation rows past M read zeros.
+  const int nkbt = K / 32;  // tiles per 16-row block
+  const int rb = 4 * cb + wave;
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)Wt, (short)0, (int)((size_t)((ncols + 15) / 16) * 16 * K * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t xres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((size_t)M * K * 2), 0x00020000);
+  const unsigned wvoff = (unsigned)((((size_t)rb * nkbt + k0 / 32) * 64 + lane) * 16);
+  // Activation batch: thread t loads chunks t + 256 j (row c / (4 U), 8 halfs
+  // at 8 (c % (4 U))), consecutive threads reading consecutive 16 bytes.
+  constexpr int XJ = XCH / 256;
+  auto xload = [&](f16x8* v, int kb0) {
+#pragma unroll
+    for (int j = 0; j < XJ; ++j) {
+      const int c = threadIdx.x + 256 * j, r = c / (4 * U), kc = c % (4 * U);
+      v[j] = __builtin_bit_cast(
+          f16x8, __builtin_amdgcn_raw_buffer_load_b128(xres, (unsigned)((r * K + k0 + 32 * kb0 + 8 * kc) * 2), 0, 0));
+    }
+  };
+  auto xstore = [&](const f16x8* v, int buf) {
+#pragma unroll
+    for (int j = 0; j < XJ; ++j) {
+      const int c = threadIdx.x + 256 * j, r = c / (4 * U), kc = c % (4 * U);
+      *reinterpret_cast<f16x8*>(&xs[buf][r * XP + 8 * kc]) = v[j];
+    }
+  };
+  auto wload = [&](f16x8* w, int kb0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      w[u] = __builtin_bit_cast(f16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, wvoff + 1024u * (kb0 + u), 0, 0));
+  };
+  f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const f16x8* w, int buf, int kb0) {
+    const _Float16* xb = &xs[buf][(lane & 15) * XP + 8 * (lane >> 4)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (kb0 + u < nkb) {
+        const f16x8 b0 = *reinterpret_cast<const f16x8*>(xb + 32 * u);
+        const f16x8 b1 = *reinterpret_cast<const f16x8*>(xb + 16 * XP + 32 * u);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(w[u], b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(w[u], b1, acc1, 0, 0, 0);
+      }
+    }
+  };
+  // Batch i computes from xs[i & 1] and registers wa / wb while batch i + 1's
+  // activations and weights load; one barrier per batch orders the LDS reuse.
+  f16x8 wa[U], wb[U], xv[XJ];
+  xload(xv, 0);
+  wload(wa, 0);
+  xstore(xv, 0);
+  __syncthreads();
+  const int nbatch = (nkb + U - 1) / U;
+  for (int bt = 0; bt < nbatch; bt += 2) {
+    if (bt + 1 < nbatch) {
+      xload(xv, (bt + 1) * U);  // issued before the weights, so waiting for it leaves them in flight
+      wload(wb, (bt + 1) * U);
+    }
+    compute(wa, 0, bt * U);
+    if (bt + 1 >= nbatch) break;
+    xstore(xv, 1);
+    __syncthreads();
+    if (bt + 2 < nbatch) {
+      xload(xv, (bt + 2) * U);
+      wload(wa, (bt + 2) * U);
+    }
+    compute(wb, 1, (bt + 1) * U);
+    if (bt + 2 >= nbatch) break;
+    xstore(xv, 0);
+    __syncthreads();
+  }
+
+  // acc0[j] of lane l: column 16 wave + 4 (l / 16) + j, row l % 16 (acc1: row + 16).
+  constexpr int LDC = 68;
+  static_assert(2 * 32 * XP * 2 >= 32 * LDC * 4, "the tile fits the activation buffers");
+  float* Cs = reinterpret_cast<float*>(&xs[0][0]);
+  __syncthreads();  // every wave is done with the activations
+  {
+    const int col = 16 * wave + 4 * (lane >> 4), r = lane & 15;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      Cs[r * LDC + col + j] = acc0[j];
+      Cs[(r + 16) * LDC + col + j] = acc1[j];
+    }
+  }
+  __syncthreads();
+  if (partial) {
+    float* dst = partial + (size_t)split * M * ncols;
+    for (int i = threadIdx.x; i < M * 64; i += 256) {
+      const int rr = i / 64, c = i % 64;
+      if (n0 + c < ncols) dst[(size_t)rr * ncols + n0 + c] = Cs[rr * LDC + c];
+    }
+    return;
+  }
+  epi(Cs, LDC, 0, M, n0, 32, 64);
+}
+
+template <class Epi>
+static int launch_skinny(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* Wt, int K,
+                         int n_cols, const Epi& e, bool defer) {
+  // Buffer ranges take 31-bit byte offsets.
+  if ((size_t)((n_cols + 15) / 16) * 16 * K * 2 >= ((size_t)1 << 31) || (size_t)32 * K * 2 >= ((size_t)1 << 31)) return 0;
+  const int nb = (n_cols + 63) / 64;
+  const int nk = K / 32;
+  // Split K only to give about 256 workgroups (at least 8 K blocks each).
+  int splits = std::max(1, std::min((256 + nb - 1) / nb, nk / 8));
+  while (splits > 1 && (size_t)splits * M * n_cols * sizeof(float) > ws.bytes) --splits;
+  const int per = (nk + splits - 1) / splits;
+  splits = (nk + per - 1) / per;
+  float* part = splits > 1 ? ws.ptr : nullptr;
+  k_gemm_skinny<Epi, 8><<<nb * splits, 256, 0, st>>>(A, M, Wt, K, nb, per, part, n_cols, e);
+  if (splits > 1 && !defer)
+    k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ((n_cols + 127) / 128), 256, 0, st>>>(
+        part, splits, M, n_cols, (n_cols + 127) / 128, e);
+  return splits;
+}
+
 // Tile choice of a prompt-sized GEMM: {BM, BN, splits}, BM == 0 for the
 // small-tile kernel.  HH_GEMM_QKV / _RESID (O projection) / _DOWN / _GATEUP =
 // "BMxBNxS" (or "0") overrides it, for tuning.
@@ -796,11 +943,15 @@ static int run_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, 
 // splits used (with defer, partials of a split run are left in ws.ptr).
 template <typename TM, class Epi>
 static int run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e,
-                    GemmKind kind, bool defer = false) {
+                    GemmKind kind, bool defer = false, const TM* Wt = nullptr) {
   if constexpr (sizeof(TM) == 2) {
     if (K % 64 == 0) {
       const _Float16* Ah = reinterpret_cast<const _Float16*>(A);
       const _Float16* Wh = reinterpret_cast<const _Float16*>(W);
+      if (M <= 32 && Wt) {
+        const int sp = launch_skinny(st, ws, Ah, M, reinterpret_cast<const _Float16*>(Wt), K, n_cols, e, defer);
+        if (sp > 0) return sp;
+      }
       if constexpr (!std::is_same<Epi, EpiLogits>::value) {
         const int sp = run_wide(st, ws, Ah, M, Wh, K, n_cols, e, kind, defer);
         if (sp > 0) return sp;
@@ -822,6 +973,7 @@ static int run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const 
 // eps) * gain in the MFMA operand type.  The row (N % 4 == 0, N <= 4096) stays
 // in registers between the two halves.
 constexpr int kNormMaxChunks = 4;  // float4 chunks per thread: N <= 4096
+constexpr int kNormSplitBatch = 8;  // split partials in flight per chunk
 template <typename TM>
 __global__ __launch_bounds__(256) void k_resid_norm(const float* __restrict__ partial, int splits, int M, int N, float scale,
                                                     float* __restrict__ x, const float* __restrict__ gain, float eps,
@@ -839,13 +991,21 @@ __global__ __launch_bounds__(256) void k_resid_norm(const float* __restrict__ pa
       if (splits > 0) {
         const float4* pp = reinterpret_cast<const float4*>(partial + (size_t)row * N) + ch;
         const size_t stride = (size_t)M * nc;  // one split's partials, in float4
+        // Up to kNormSplitBatch partials are loaded at once (clamped indices,
+        // unused ones dropped), then summed in split order.
         float4 t = pp[0];
-        for (int sp = 1; sp < splits; ++sp) {
-          const float4 u = pp[sp * stride];
-          t.x += u.x;
-          t.y += u.y;
-          t.z += u.z;
-          t.w += u.w;
+        for (int s0 = 1; s0 < splits; s0 += kNormSplitBatch) {
+          float4 u[kNormSplitBatch];
+#pragma unroll
+          for (int j = 0; j < kNormSplitBatch; ++j) u[j] = pp[min(s0 + j, splits - 1) * stride];
+#pragma unroll
+          for (int j = 0; j < kNormSplitBatch; ++j)
+            if (s0 + j < splits) {
+              t.x += u[j].x;
+              t.y += u[j].y;
+              t.z += u[j].z;
+              t.w += u[j].w;
+            }
         }
         a.x += t.x * scale;
         a.y += t.y * scale;
@@ -880,9 +1040,9 @@ __global__ __launch_bounds__(256) void k_resid_norm(const float* __restrict__ pa
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::qkv(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
                                const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM,
-                               TKV* kv, KvLayout L, int layer, const int* page_table) {
+                               TKV* kv, KvLayout L, int layer, const int* page_table, const TM* Wt) {
   EpiQKV<TKV> e{hq, hkv, scale, row_stream, row_pos, rope, q, reinterpret_cast<TKV*>(qM), kv, L, layer, page_table};
-  run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e, GemmKind::QKV);
+  run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e, GemmKind::QKV, false, Wt);
 }
 
 template <typename TM, typename TKV>
@@ -892,10 +1052,10 @@ bool GemmKernels<TM, TKV>::norm_fusable(int N) {
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale,
-                                 float* x, const float* gain, float eps, TM* h) {
+                                 float* x, const float* gain, float eps, TM* h, const TM* Wt) {
   EpiResid e{N, scale, x};
   const bool norm = gain != nullptr;
-  const int sp = run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid, norm);
+  const int sp = run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid, norm, Wt);
   if (norm) k_resid_norm<TM><<<M, 256, 0, st>>>(ws.ptr, sp > 1 ? sp : 0, M, N, scale, x, gain, eps, h);
 }
 
@@ -906,17 +1066,17 @@ void GemmKernels<TM, TKV>::rmsnorm(hipStream_t st, int M, float* x, int N, const
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale,
-                                  TM* m) {
+                                  TM* m, const TM* Wt) {
   // Groups of 32 gate + 32 up columns: every tile width here is a multiple of 64.
   EpiGateUp<TM> e{F, 32, scale, m};
-  run_gemm<TM>(st, ws, A, M, W, d, ((F + 31) / 32) * 64, e, GemmKind::GateUp);
+  run_gemm<TM>(st, ws, A, M, W, d, ((F + 31) / 32) * 64, e, GemmKind::GateUp, false, Wt);
 }
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale,
-                                  float* logits, unsigned long long* slot, const int* row_stream) {
+                                  float* logits, unsigned long long* slot, const int* row_stream, const TM* Wt) {
   EpiLogits e{V, scale, logits, slot, row_stream};
-  run_gemm<TM>(st, ws, A, M, W, d, V, e, GemmKind::Logits);
+  run_gemm<TM>(st, ws, A, M, W, d, V, e, GemmKind::Logits, false, Wt);
 }
 
 template struct GemmKernels<float, float>;

@@ -65,6 +65,35 @@ void transpose(hipStream_t st, const T* src, T* dst, int rows, int cols) {
   dim3 grid((cols + 31) / 32, (rows + 31) / 32);
   k_transpose<T><<<grid, 256, 0, st>>>(src, dst, rows, cols);
 }
+// Operand tiles for the 32-row GEMM: dst[(rb * (K / 32) + kb) * 64 + l] (16
+// bytes each) = row 16 rb + l % 16, columns 32 kb + 8 (l / 16) .. + 8 of the
+// logical matrix, whose row n is source row n (interleave_f == 0) or, for
+// the gate/up matrix in groups of 32 gate + 32 up rows, row j or F + j with
+// j = 32 (n / 64) + n % 32 (interleave_f == F); rows past the matrix are zero.
+__global__ void k_tile16(const _Float16* __restrict__ src, _Float16* __restrict__ dst, int rows, int K, int interleave_f,
+                         size_t n_chunks) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_chunks) return;
+  const int l = (int)(i & 63);
+  const size_t t = i >> 6;
+  const int nkb = K / 32;
+  const int kb = (int)(t % nkb), rb = (int)(t / nkb);
+  const int n = 16 * rb + (l & 15), k = 32 * kb + 8 * (l >> 4);
+  int row = n;
+  if (interleave_f > 0) {
+    const int c = n & 63, j = (n >> 6) * 32 + (c & 31);
+    row = j < interleave_f ? (c < 32 ? j : interleave_f + j) : -1;
+  }
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (row >= 0 && row < rows) v = *reinterpret_cast<const u32x4*>(src + (size_t)row * K + k);
+  reinterpret_cast<u32x4*>(dst)[i] = v;
+}
+
+void tile16(hipStream_t st, const _Float16* src, _Float16* dst, int rows, int K, int logical_rows, int interleave_f) {
+  const size_t n_chunks = (size_t)((logical_rows + 15) / 16) * 16 * K / 8;
+  k_tile16<<<(unsigned)((n_chunks + 255) / 256), 256, 0, st>>>(src, dst, rows, K, interleave_f, n_chunks);
+}
+
 template void transpose<__bf16>(hipStream_t, const __bf16*, __bf16*, int, int);
 template void transpose<float>(hipStream_t, const float*, float*, int, int);
 template void transpose<_Float16>(hipStream_t, const _Float16*, _Float16*, int, int);

@@ -35,6 +35,10 @@ struct Layout {
   // byte offsets into the arena
   size_t embed, lm_head, embedM, lm_headM;
   std::vector<size_t> wqkv, wo, wgu, wdown, wdownT, wqkvM, woM, wguM, wdownM, attn_norm, mlp_norm;
+  // 16 x 32 operand tiles of the fp16 copies for <= 32-row GEMMs (multi-stream
+  // contexts of bf16 models only; empty otherwise).
+  std::vector<size_t> wqkvT16, woT16, wguT16, wdownT16;
+  size_t lm_headT16;
   size_t final_norm, rope, kv, page_table, pos, pending, slot, hist, ll, ll_words, layer_tab, trace;
   size_t row_stream, row_pos, feed, x, h, q, qM, o32, oM, m32, mM, part, logits, gemm_ws, gemm_ws_bytes, scratch_u32;
   size_t total;
@@ -94,6 +98,16 @@ Layout make_layout(const hh_config& c) {
       L.woM.push_back(take(d * hq * 64 * L.em));
       L.wguM.push_back(take(2 * F * d * L.em));
       L.wdownM.push_back(take(d * F * L.em));
+    }
+    if (c.max_streams > 1) {
+      auto tiles = [&](size_t logical_rows, size_t K) { return take((logical_rows + 15) / 16 * 16 * K * 2); };
+      L.lm_headT16 = tiles(V, d);
+      for (int l = 0; l < c.n_layers; ++l) {
+        L.wqkvT16.push_back(tiles(L.nqkv, d));
+        L.woT16.push_back(tiles(d, hq * 64));
+        L.wguT16.push_back(tiles((F + 31) / 32 * 64, d));
+        L.wdownT16.push_back(tiles(d, F));
+      }
     }
   } else {
     L.embedM = L.embed;
@@ -249,8 +263,9 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       // Prefill rows of one stream with an fp16 cache use MFMA flash attention.
       const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv, c->cfg.max_context);
       // Flash attention reads only the fp16 queries.
+      const bool tiled = !L.wqkvT16.empty();
       GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, flash ? nullptr : q,
-              flash ? c->at<TM>(L.qM) : nullptr, kv, kl, l, pt);
+              flash ? c->at<TM>(L.qM) : nullptr, kv, kl, l, pt, tiled ? c->at<TM>(L.wqkvT16[l]) : nullptr);
       if (flash) {
         if constexpr (sizeof(TKV) == 2)
           flash_prefill(st, reinterpret_cast<const _Float16*>(c->at<TM>(L.qM)), reinterpret_cast<const _Float16*>(kv),
@@ -260,15 +275,17 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       } else {
         DK::attention_rows(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, o32, oM);
       }
+      const TM* wo_t = tiled ? c->at<TM>(L.woT16[l]) : nullptr;
       if (fuse) {
-        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h);
+        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h, wo_t);
       } else {
-        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x);
+        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, nullptr, 0.f, nullptr, wo_t);
         DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
       }
-      GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM);
+      GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM, tiled ? c->at<TM>(L.wguT16[l]) : nullptr);
       const float* next_an = (fuse && l + 1 < g.n_layers) ? c->at<float>(L.attn_norm[l + 1]) : nullptr;
-      GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h);
+      GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h,
+                tiled ? c->at<TM>(L.wdownT16[l]) : nullptr);
     }
   }
   const float* fn = c->at<float>(L.final_norm);
@@ -281,7 +298,8 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       TM* h = c->at<TM>(L.h);
       if (GK::norm_fusable(d)) GK::rmsnorm(st, n, x, d, fn, eps, h);
       else DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
-      GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs);
+      GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs,
+                 L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16));
     }
   }
 }
@@ -662,6 +680,16 @@ hh_status hh_load_weights(hh_ctx* c, const void* const* tensors, int32_t n_tenso
     // Wdown^T of the fp16 copy, for the batch-1 decode kernel's split-K down projection.
     for (int l = 0; l < g.n_layers; ++l)
       transpose(st, c->at<_Float16>(L.wdownM[l]), c->at<_Float16>(L.wdownT[l]), (int)d, (int)F);
+    if (!L.wqkvT16.empty()) {
+      tile16(st, c->at<_Float16>(L.lm_headM), c->at<_Float16>(L.lm_headT16), (int)V, (int)d, (int)V, 0);
+      for (int l = 0; l < g.n_layers; ++l) {
+        tile16(st, c->at<_Float16>(L.wqkvM[l]), c->at<_Float16>(L.wqkvT16[l]), L.nqkv, (int)d, L.nqkv, 0);
+        tile16(st, c->at<_Float16>(L.woM[l]), c->at<_Float16>(L.woT16[l]), (int)d, (int)(hq * 64), (int)d, 0);
+        tile16(st, c->at<_Float16>(L.wguM[l]), c->at<_Float16>(L.wguT16[l]), (int)(2 * F), (int)d,
+               (int)((F + 31) / 32 * 64), (int)F);
+        tile16(st, c->at<_Float16>(L.wdownM[l]), c->at<_Float16>(L.wdownT16[l]), (int)d, (int)F, (int)d, 0);
+      }
+    }
   } else {
     c->wscale = 1.f;
   }
