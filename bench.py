@@ -91,6 +91,75 @@ def cpu_baseline(shape, wseed, prompt, n_decode):
     return n_decode / (t2 - t1), t1 - t0, cores
 
 
+def measure_others(ctx, shape, st, names):
+    """The other workloads on the same context: 1024-token TTFT, decode over
+    8192 cached positions, 32-stream lockstep decode."""
+    import torch
+
+    import synth
+    from paper_2606_12154_amd import hh
+    other = {}
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    if "prompt1024" in names:
+        # 1024-token prompt: TTFT (the prefill-dominated workload), then 64 steps.
+        w3 = synth.WORKLOADS["1b_prefill"]
+        p3 = synth.make_tokens(shape.vocab, w3["prompt"], w3["tseed"])
+        tt = []
+        for i in range(4):
+            ctx.reset(0)
+            t0 = time.perf_counter()
+            ctx.prefill(0, p3)
+            if i:
+                tt.append(time.perf_counter() - t0)
+        e0.record(st)
+        for _ in range(w3["steps"]):
+            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        other["prompt1024"] = {"ttft_ms": round(float(np.mean(tt)) * 1e3, 3),
+                               "ttft_ms_min": round(float(np.min(tt)) * 1e3, 3),
+                               "prefill_tflops": round(2.062e12 / float(np.mean(tt)) / 1e12, 1),
+                               "decode_tok_s": round(w3["steps"] / (e0.elapsed_time(e1) / 1e3), 1)}
+
+    if "cache8192" in names:
+        # 8192 positions already cached (untimed prefill), then 512 decode steps.
+        w4 = synth.WORKLOADS["1b_long"]
+        ctx.reset(0)
+        ctx.prefill(0, synth.make_tokens(shape.vocab, w4["prompt"], w4["tseed"]))
+        e0.record(st)
+        for _ in range(w4["steps"]):
+            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        s4 = e0.elapsed_time(e1) / 1e3
+        t4 = w4["prompt"] + (w4["steps"] - 1) / 2.0 + 1
+        b4 = decode_step_bytes(shape, t4)
+        other["cache8192"] = {"decode_tok_s": round(w4["steps"] / s4, 1),
+                              "hbm_frac": round(b4 * w4["steps"] / s4 / 1e9 / HBM_PEAK_GBS, 4)}
+
+    if "streams32" in names:
+        # 32 independent streams, 256-token prompts, lockstep decode.
+        w5 = synth.WORKLOADS["1b_multi"]
+        ctx.reset(-1)
+        ns = w5["streams"]
+        for s_ in range(ns):
+            ctx.prefill(s_, synth.make_tokens(shape.vocab, w5["prompt"], w5["tseed"] + s_))
+        hh.hh_decode_step(ctx.ctx, ns, None, None, None, None)  # first step captures the graph
+        e0.record(st)
+        n5 = w5["steps"] - 1
+        for _ in range(n5):
+            hh.hh_decode_step(ctx.ctx, ns, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        s5 = e0.elapsed_time(e1) / 1e3
+        t5 = w5["prompt"] + 1 + n5 / 2.0 + 1
+        b5 = shape.n_params() * 2 + ns * kv_bytes_per_position(shape) * (t5 + 1)
+        other["streams32"] = {"aggregate_tok_s": round(ns * n5 / s5, 1), "step_ms": round(s5 / n5 * 1e3, 3),
+                              "hbm_frac": round(b5 * n5 / s5 / 1e9 / HBM_PEAK_GBS, 4)}
+    return other
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -99,6 +168,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--other-configs", action="store_true",
                     help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
+    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32"],
+                    help="measure just this one of the other workloads (for a kernel trace of it); "
+                         "prints its figures instead of the decode line")
     ap.add_argument("--cpu-decode-steps", type=int, default=8)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
@@ -144,6 +216,12 @@ def main():
         e1.synchronize()
         return ttft, e0.elapsed_time(e1) / 1e3
 
+    if args.only:
+        other = measure_others(ctx, shape, st, [args.only])
+        print(json.dumps({"metric": METRIC, "workload": args.only, "data": "synthetic", "n_gpus": 1,
+                          **other[args.only]}), flush=True)
+        ctx.close()
+        return
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
@@ -194,61 +272,7 @@ def main():
     }
 
     if args.other_configs:
-        other = {}
-        # 1024-token prompt: TTFT (the prefill-dominated workload), then 64 steps.
-        w3 = synth.WORKLOADS["1b_prefill"]
-        p3 = synth.make_tokens(shape.vocab, w3["prompt"], w3["tseed"])
-        tt = []
-        for i in range(4):
-            ctx.reset(0)
-            t0 = time.perf_counter()
-            ctx.prefill(0, p3)
-            if i:
-                tt.append(time.perf_counter() - t0)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(st)
-        for _ in range(w3["steps"]):
-            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
-        e1.record(st)
-        e1.synchronize()
-        other["prompt1024"] = {"ttft_ms": round(float(np.mean(tt)) * 1e3, 3),
-                               "ttft_ms_min": round(float(np.min(tt)) * 1e3, 3),
-                               "prefill_tflops": round(2.062e12 / float(np.mean(tt)) / 1e12, 1),
-                               "decode_tok_s": round(w3["steps"] / (e0.elapsed_time(e1) / 1e3), 1)}
-        # 8192 positions already cached (untimed prefill), then 512 decode steps.
-        w4 = synth.WORKLOADS["1b_long"]
-        ctx.reset(0)
-        ctx.prefill(0, synth.make_tokens(shape.vocab, w4["prompt"], w4["tseed"]))
-        e0.record(st)
-        for _ in range(w4["steps"]):
-            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
-        e1.record(st)
-        e1.synchronize()
-        s4 = e0.elapsed_time(e1) / 1e3
-        t4 = w4["prompt"] + (w4["steps"] - 1) / 2.0 + 1
-        b4 = decode_step_bytes(shape, t4)
-        other["cache8192"] = {"decode_tok_s": round(w4["steps"] / s4, 1),
-                              "hbm_frac": round(b4 * w4["steps"] / s4 / 1e9 / HBM_PEAK_GBS, 4)}
-        # 32 independent streams, 256-token prompts, lockstep decode.
-        w5 = synth.WORKLOADS["1b_multi"]
-        ctx.reset(-1)
-        ns = w5["streams"]
-        for s_ in range(ns):
-            ctx.prefill(s_, synth.make_tokens(shape.vocab, w5["prompt"], w5["tseed"] + s_))
-        hh.hh_decode_step(ctx.ctx, ns, None, None, None, None)  # first step captures the graph
-        e0.record(st)
-        n5 = w5["steps"] - 1
-        for _ in range(n5):
-            hh.hh_decode_step(ctx.ctx, ns, None, None, None, None)
-        e1.record(st)
-        e1.synchronize()
-        s5 = e0.elapsed_time(e1) / 1e3
-        t5 = w5["prompt"] + 1 + n5 / 2.0 + 1
-        b5 = shape.n_params() * 2 + ns * kv_bytes_per_position(shape) * (t5 + 1)
-        other["streams32"] = {"aggregate_tok_s": round(ns * n5 / s5, 1), "step_ms": round(s5 / n5 * 1e3, 3),
-                              "hbm_frac": round(b5 * n5 / s5 / 1e9 / HBM_PEAK_GBS, 4)}
-        out["other_configs"] = other
+        out["other_configs"] = measure_others(ctx, shape, st, ["prompt1024", "cache8192", "streams32"])
 
     ctx.close()
     del ctx
