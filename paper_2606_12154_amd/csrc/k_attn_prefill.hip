@@ -144,12 +144,14 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     // appended chunk: keep such a query's state at (-inf, 0, 0).
     const float mn = fmaxf(m, bm);
     const float mref = mn == -INFINITY ? 0.f : mn;
-    const float alpha = exp2f(m - mref);
+    // Hardware exp2 (arguments are <= 0; results below the normal range flush
+    // to zero, which a softmax weight can take).
+    const float alpha = __builtin_amdgcn_exp2f(m - mref);
     float ls = 0.f;
     f16x8 pb[2];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float pv = exp2f(sacc[i] - mref);
+      const float pv = __builtin_amdgcn_exp2f(sacc[i] - mref);
       ls += pv;
       pb[i >> 3][i & 7] = (_Float16)pv;
     }
@@ -178,17 +180,25 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     m = mn;
   };
 
-  // Two register sets in rotation: block it + 1 is in flight while block it
-  // is processed (loads of absent blocks are clamped, never used).
-  KvRegs A, B;
+  // Three register sets in rotation: blocks it + 1 and it + 2 are in flight
+  // while block it is processed (loads of absent blocks are clamped, never
+  // used).
+  KvRegs R0, R1, R2;
   const int kcl = (nkb - 1) * 32;
-  if (idx < 256) flash_load(A, kv, L, layer, pt, g, idx, min(grp * 32, kcl), kend);
-  for (int it = 0; it < niter; it += 2) {
-    if (idx < 256) flash_load(B, kv, L, layer, pt, g, idx, min(((it + 1) * NS + grp) * 32, kcl), kend);
-    process(A, it);
+  auto blk = [&](int it) { return min((it * NS + grp) * 32, kcl); };
+  if (idx < 256) {
+    flash_load(R0, kv, L, layer, pt, g, idx, blk(0), kend);
+    flash_load(R1, kv, L, layer, pt, g, idx, blk(1), kend);
+  }
+  for (int it = 0; it < niter; it += 3) {
+    if (idx < 256) flash_load(R2, kv, L, layer, pt, g, idx, blk(it + 2), kend);
+    process(R0, it);
     if (it + 1 >= niter) break;
-    if (idx < 256) flash_load(A, kv, L, layer, pt, g, idx, min(((it + 2) * NS + grp) * 32, kcl), kend);
-    process(B, it + 1);
+    if (idx < 256) flash_load(R0, kv, L, layer, pt, g, idx, blk(it + 3), kend);
+    process(R1, it + 1);
+    if (it + 2 >= niter) break;
+    if (idx < 256) flash_load(R1, kv, L, layer, pt, g, idx, blk(it + 4), kend);
+    process(R2, it + 2);
   }
   lsum += __shfl_xor(lsum, 32, 64);
 
@@ -212,7 +222,7 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     float mx = m;
 #pragma unroll
     for (int sp = 1; sp < NS; ++sp) mx = fmaxf(mx, mg[((sp - 1) * G + hi) * (2 + 32) * 64 + lane]);
-    const float w0 = exp2f(m - mx);
+    const float w0 = __builtin_amdgcn_exp2f(m - mx);
     lsum *= w0;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -222,7 +232,7 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
 #pragma unroll
     for (int sp = 1; sp < NS; ++sp) {
       const float* r = mg + ((sp - 1) * G + hi) * (2 + 32) * 64;
-      const float w = exp2f(r[lane] - mx);  // 0 for a split that saw no key
+      const float w = __builtin_amdgcn_exp2f(r[lane] - mx);  // 0 for a split that saw no key
       lsum += w * r[64 + lane];
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
