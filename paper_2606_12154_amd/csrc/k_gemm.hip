@@ -754,15 +754,16 @@ static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
 
 // Lockstep multi-stream decode: C[M <= 32, N] = A W^T is weight streaming, not
 // arithmetic.  A workgroup owns 64 logical columns (one QKV head, 32 gate + 32
-// up columns, or 64 residual columns) and one K range; its four waves take 16
-// weight rows each.  Weights go from HBM straight into registers as the A
-// operand of 16x16x32 MFMAs (lane l: row l%16, k 8(l/16) .. + 8), in
-// batches of eight K blocks with the next batch loading while one computes;
-// the activations (at most 32 rows) of each batch are loaded once per
-// workgroup, coalesced, into double-buffered LDS (16-byte row padding keeps
-// the B fragment reads conflict-free).  The finished
-// 64-column tile goes through LDS into the usual epilogue, or into split
-// partials when K is split to give every CU work.
+// up columns, or 64 residual columns) and one K range; each group of four
+// waves takes 16 weight rows per wave (KW groups split the K range).  Weights
+// go from HBM straight into registers as the A operand of 16x16x32 MFMAs (lane
+// l: row l%16, k 8(l/16) .. + 8), from a copy laid out as 16 x 32 operand
+// tiles, in batches of eight K blocks with the next batch loading while one
+// computes; the activations (at most 32 rows) of each batch are loaded once per
+// K group, coalesced, into double-buffered LDS (16-byte row padding keeps the
+// B fragment reads conflict-free).  The finished 64-column tile goes through
+// LDS into the usual epilogue, or into split partials when K is split to give
+// every CU work.
 template <class Epi, int U, int KW>
 __global__ __launch_bounds__(256 * KW) void k_gemm_skinny(const _Float16* __restrict__ A, int M,
                                                           const _Float16* __restrict__ Wt, int K, int nb,
