@@ -872,15 +872,16 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
           char* slot = ring + (size_t)pos * kSlot;
           // The slot holding this step's position gets the exchanged key and
           // value (its cache row may not have been written yet when it was
-          // streamed); rows past the item's last key get zero values (stale
-          // or foreign slots: weight 0, and 0 * NaN would be NaN).
+          // streamed) -- also when that position is the slot's last row;
+          // rows past the item's last key get zero values (stale or foreign
+          // slots: weight 0, and 0 * NaN would be NaN).
+          if (p >= key0 && p < key0 + 32 && p < kend) {
+            const int kk = p - key0, tt = kk >> 4, key = kk & 15;
+            const int off = tt * 4096 + key * 128 + ((((lane >> 3) ^ ((key >> 1) & 7))) << 4) + (lane & 7) * 2;
+            *reinterpret_cast<_Float16*>(slot + off) = (_Float16)kn[lane];
+            *reinterpret_cast<_Float16*>(slot + off + 2048) = (_Float16)vn[lane];
+          }
           if (key0 + 32 > kend) {
-            if (p >= key0 && p < kend) {
-              const int kk = p - key0, tt = kk >> 4, key = kk & 15;
-              const int off = tt * 4096 + key * 128 + ((((lane >> 3) ^ ((key >> 1) & 7))) << 4) + (lane & 7) * 2;
-              *reinterpret_cast<_Float16*>(slot + off) = (_Float16)kn[lane];
-              *reinterpret_cast<_Float16*>(slot + off + 2048) = (_Float16)vn[lane];
-            }
             for (int r = kend - key0 + (lane >> 3); r < 32; r += 8)
               *reinterpret_cast<u32x4*>(slot + (r >> 4) * 4096 + 2048 + (r & 15) * 128 + (lane & 7) * 16) =
                   u32x4{0u, 0u, 0u, 0u};
