@@ -933,12 +933,13 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
     return WideCfg{0, 0, 1};
   }
   // Measured on the 1B prompt shapes (d 2048, FFN 8192): gate/up at 1024 rows
-  // 88.9 -> ~72 us with 256 x 256 tiles (256 tiles, one per CU); the down
-  // and O projections (only 128 tiles of 128 x 128) gain most from a 2-way K
-  // split; QKV, and everything at 256 rows, stay on the small-tile kernel,
-  // whose two workgroups per CU suit these few-tile shapes better.
+  // takes 256 x 128 tiles (512 tiles, two rounds of the CUs; TTFT 3.74 ->
+  // 3.44 ms against 256 x 256, one tile per CU); the down and O projections
+  // (only 128 tiles of 128 x 128) gain most from a 2-way K split; QKV, and
+  // everything at 256 rows, stay on the small-tile kernel, whose two
+  // workgroups per CU suit these few-tile shapes better.
   if (kind == GemmKind::GateUp && n_cols >= 8192) {
-    if (M >= 512) return WideCfg{256, 256, 1};
+    if (M >= 512) return WideCfg{256, 128, 1};
     if (M >= 256) return WideCfg{128, 128, 1};
   }
   if (kind == GemmKind::Resid && M >= 512) return WideCfg{128, 128, 2};
