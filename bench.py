@@ -160,6 +160,44 @@ def measure_others(ctx, shape, st, names):
     return other
 
 
+def measure_ctx_sweep(shape):
+    """Decode rate against the number of cached positions (the paper's window
+    sweep, here over positions actually attended): a 1-stream context of
+    32768 positions; for each length a seeded prompt fills the cache
+    (untimed), then 64 device-fed decode steps are timed."""
+    import torch
+
+    import synth
+    from paper_2606_12154_amd import hh
+    steps = 64
+    tensors = synth.make_weights(shape, synth.WORKLOADS["1b_decode"]["wseed"])
+    ctx = hh.Context(hh.make_config(shape, 1, 32768, 8192))
+    ctx.load_weights(tensors)
+    del tensors
+    st = ctx.stream
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    rows = []
+    for n in (1024, 2048, 4096, 8192, 16384, 32768 - steps):
+        ctx.reset(0)
+        ctx.prefill(0, synth.make_tokens(shape.vocab, n, 500 + n))
+        hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e0.record(st)
+        for _ in range(steps - 1):
+            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        sec = e0.elapsed_time(e1) / 1e3
+        t = n + 1 + (steps - 2) / 2.0 + 1
+        b = decode_step_bytes(shape, t)
+        rows.append({"cached": n, "decode_tok_s": round((steps - 1) / sec, 1),
+                     "ms_per_token": round(sec / (steps - 1) * 1e3, 4),
+                     "hbm_frac": round(b * (steps - 1) / sec / 1e9 / HBM_PEAK_GBS, 4)})
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+    ctx.close()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,7 +206,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--other-configs", action="store_true",
                     help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
-    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32"],
+    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep"],
                     help="measure just this one of the other workloads (for a kernel trace of it); "
                          "prints its figures instead of the decode line")
     ap.add_argument("--cpu-decode-steps", type=int, default=8)
@@ -187,6 +225,11 @@ def main():
 
     wl = synth.WORKLOADS["1b_decode"]
     shape, P, N = wl["shape"], wl["prompt"], wl["steps"]
+    if args.only == "ctxsweep":
+        rows = measure_ctx_sweep(shape)
+        print(json.dumps({"metric": METRIC, "workload": "ctxsweep", "data": "synthetic", "n_gpus": 1,
+                          "decode_vs_cached_positions": rows}), flush=True)
+        return
     prompt = synth.make_tokens(shape.vocab, P, wl["tseed"])
     tensors = synth.make_weights(shape, wl["wseed"])
     # One context serves every 1B workload: 32 streams, 8192 + 512 positions.

@@ -7,9 +7,10 @@
 * 1B bf16 model, 32 streams in lockstep (the multi-stream workload's stream
   count) with ragged prompt lengths, one of a single token: every row's
   logits within 2e-2 of the oracle.
-* 1B bf16 model, an 8192-position prompt (the long-context workload): the
-  prompt is beyond what the oracle evaluates in test time, so the check is a
-  property that holds at any size: the batch-1 decode kernel and the
+* 1B bf16 model, 8192- and 32760-position prompts (the long-context workload
+  and the largest supported context): the prompt is beyond what the oracle
+  evaluates in test time, so the check is a property that holds at any size:
+  the batch-1 decode kernel and the
   independent GEMM / graph decode path (selected with HH_STEP_KERNEL=0) agree
   on every logit within 2e-2 and on the greedy token wherever the top-2
   margin exceeds 2e-2.
@@ -74,9 +75,9 @@ def test_1b_32_streams_lockstep(one_b):
         ctx.close()
 
 
-def test_1b_8192_positions_kernel_paths_agree(one_b):
+@pytest.mark.parametrize("P", [8192, 32760])
+def test_1b_long_context_kernel_paths_agree(one_b, P):
     shape, tensors = one_b
-    P = 8192
     toks = synth.make_tokens(shape.vocab, P + 3, 4)
     step_ctx = new_context(shape, tensors, streams=1, context=P + 8, max_prefill=2048)
     os.environ["HH_STEP_KERNEL"] = "0"
@@ -98,7 +99,7 @@ def test_1b_8192_positions_kernel_paths_agree(one_b):
             assert d <= 2e-2, f"paths differ by {d:.3g}"
             if top2_margin(b) > 2e-2:
                 assert int(np.argmax(a)) == int(np.argmax(b))
-        print(f"1B decode at 8192 positions, kernel vs graph path: max-abs {worst:.3g}")
+        print(f"1B decode at {P} positions, kernel vs graph path: max-abs {worst:.3g}")
     finally:
         step_ctx.close()
         graph_ctx.close()
