@@ -21,11 +21,16 @@ Pins (``tests/test_oracle.py``): closed-form RMSNorm/RoPE/SiLU values, fp64
 brute-force attention on tiny shapes, GQA == MHA with repeated KV heads, the
 HuggingFace transformers Llama implementation on the tiny model, causality,
 KV-cached decode == full recompute, chunked == one-shot prefill, and the
-zero-layer echo model.  Matching the paper's own model outputs is parity
-unpinned: its weights and printed outputs do not exist.
+zero-layer echo model; for the 4-bit group format (``quant.py``): a worked
+example, exact round trips of representable groups, the half-step error
+bound, ties to even, zero groups and the nibble layout.  Matching the paper's
+own model outputs is parity unpinned: its weights and printed outputs do not
+exist, and neither does its 4-bit format's definition.
 """
 from .decoder import (Decoder, KVCache, apply_rope, attention, greedy, rms_norm,
                       rope_angles, silu)
+from .quant import q4_dequantize, q4_model_weights, q4_pack_rows, q4_quantize_rows
 
 __all__ = ["Decoder", "KVCache", "apply_rope", "attention", "greedy", "rms_norm",
-           "rope_angles", "silu"]
+           "rope_angles", "silu", "q4_quantize_rows", "q4_dequantize", "q4_pack_rows",
+           "q4_model_weights"]

@@ -251,3 +251,92 @@ def test_zero_layer_model_echoes_its_input():
 
 def test_greedy_ties_take_lowest_index():
     assert oracle.greedy(np.array([1.0, 3.0, 2.0, 3.0])) == 1
+
+
+# ---------------------------------------------------------------- 4-bit group format (oracle/quant.py)
+
+def test_q4_worked_example():
+    """Hand-computed: a = 0.7, a / 7 = 0.1 in fp32 (0x3DCCCCCD) rounds up to the
+    bf16 0x3DCD = 0.10009765625; 0.7 / s = 6.993 -> 7, -0.35 / s = -3.497 -> -3,
+    0.1 / s = 0.999 -> 1."""
+    w = np.zeros((1, 32), np.float32)
+    w[0, :3] = [0.7, -0.35, 0.1]
+    q, s = oracle.q4_quantize_rows(w)
+    assert s.shape == (1, 1) and s[0, 0] == np.float32(0.10009765625)
+    assert q[0, :4].tolist() == [7, -3, 1, 0] and not q[0, 4:].any()
+    d = oracle.q4_dequantize(q, s)
+    assert d[0, :3].tolist() == [0.70068359375, -0.30029296875, 0.10009765625]
+
+
+def test_q4_representable_groups_round_trip():
+    rng = np.random.default_rng(3)
+    k = rng.integers(-7, 8, size=(5, 64))
+    k[:, 0] = 7          # every group reaches |k| = 7 ...
+    k[:, 32] = -7        # ... so its scale is exactly s
+    s = np.float32(2.0 ** -6)
+    w = (k * s).astype(np.float32)
+    q, sc = oracle.q4_quantize_rows(w)
+    assert np.all(sc == s)
+    assert np.array_equal(q, k)
+    assert np.array_equal(oracle.q4_dequantize(q, sc), w.astype(np.float64))
+
+
+def test_q4_error_bound_and_range():
+    rng = np.random.default_rng(4)
+    w = (0.02 * rng.standard_normal((64, 256))).astype(np.float32)
+    w[3, 32:64] *= 1e-6     # a group of tiny values
+    q, s = oracle.q4_quantize_rows(w)
+    assert q.min() >= -7 and q.max() <= 7     # the scale never lets a value reach -8
+    err = np.abs(oracle.q4_dequantize(q, s) - w.astype(np.float64))
+    bound = np.repeat(s.astype(np.float64), 32, axis=1) / 2 * (1 + 1e-6)
+    assert np.all(err <= bound)
+    # Each group's largest magnitude maps to +-7 (to +-6 only if the bf16
+    # scale rounded up past a / 6.5, which cannot happen: a / 7 < a / 6.5).
+    g = np.abs(q.reshape(64, -1, 32)).max(axis=-1)
+    assert np.all(g == 7)
+
+
+def test_q4_ties_to_even_and_zero_group():
+    w = np.zeros((2, 32), np.float32)
+    w[0, :5] = [2.5, 3.5, -2.5, -0.5, 7.0]     # a = 7 -> s = 1 exactly
+    q, s = oracle.q4_quantize_rows(w)
+    assert s[0, 0] == 1.0 and q[0, :5].tolist() == [2, 4, -2, 0, 7]
+    assert s[1, 0] == 0.0 and not q[1].any()
+    assert not oracle.q4_dequantize(q, s)[1].any()
+
+
+def test_q4_pack_layout():
+    q = np.zeros((1, 64), np.int8)
+    q[0, :4] = [-8, 7, 0, 1]
+    s = np.array([[1.0, 0.10009765625]], np.float32)
+    b = oracle.q4_pack_rows(q, s)
+    assert b.shape == (1, 32 + 4)
+    assert b[0, :2].tolist() == [0xF0, 0x98]             # (0 | 15 << 4), (8 | 9 << 4)
+    assert np.all(b[0, 2:32] == 0x88)                    # zeros are nibble 8
+    assert b[0, 32:].tolist() == [0x80, 0x3F, 0xCD, 0x3D]  # bf16 1.0 = 0x3F80, 0.1000977 = 0x3DCD
+
+
+def test_q4_model_weights_groups():
+    """W_down is grouped along its output rows (the rows of W_down^T), the other
+    matrices along their input columns; the head is Q4(embed), the embedding
+    table and gains untouched."""
+    shape = synth.TINY
+    w = synth.weights_as_f64(shape, synth.make_weights(shape, 0, gain_std=0.1))
+    qw = oracle.q4_model_weights(shape, w)
+    assert np.array_equal(qw["embed"], w["embed"]) and np.array_equal(qw["l0.attn_norm"], w["l0.attn_norm"])
+    q, s = oracle.q4_quantize_rows(w["embed"].astype(np.float32))
+    assert np.array_equal(qw["lm_head"], oracle.q4_dequantize(q, s))
+    q, s = oracle.q4_quantize_rows(w["l1.w_down"].T.astype(np.float32))
+    assert np.array_equal(qw["l1.w_down"], oracle.q4_dequantize(q, s).T)
+    q, s = oracle.q4_quantize_rows(w["l1.wo"].astype(np.float32))
+    assert np.array_equal(qw["l1.wo"], oracle.q4_dequantize(q, s))
+    # A W_down whose columns are representable per 32 output rows is kept
+    # exactly; the same matrix grouped along its rows would not be.
+    k = np.random.default_rng(5).integers(-7, 8, size=(256, 688))
+    k[::32, :] = 7
+    wd = k * 2.0 ** -7
+    w2 = dict(w)
+    w2["l0.w_down"] = wd
+    assert np.array_equal(oracle.q4_model_weights(shape, w2)["l0.w_down"], wd)
+    qr, sr = oracle.q4_quantize_rows(wd[:, :672].astype(np.float32))
+    assert not np.array_equal(oracle.q4_dequantize(qr, sr), wd[:, :672])
