@@ -46,6 +46,20 @@ enum {
 };
 
 enum { HH_F32 = 0, HH_BF16 = 1 };                       /* weight / KV element type */
+/*
+ * Weight formats.  HH_WF_DTYPE: the weights are used as loaded (cfg.dtype).
+ * HH_WF_Q4G32 (bf16 models only): the paper's mouth model runs 4-bit weights
+ * (Sec. 4 "Runtime phase", Sec. 5) without naming the format; this library's
+ * 4-bit format is symmetric per group of 32 consecutive elements of a row:
+ * scale s = bf16(max|w| / 7) (fp32 division, round to nearest even), codes
+ * q = clamp(rint(w / s), -8, 7) (fp32 division, ties to even), value q * s.
+ * At load the bf16 matrices are quantized row by row (W_q, W_k, W_v, W_o,
+ * W_gate, W_up along their input dimension, W_down along its output
+ * dimension, i.e. the rows of W_down^T, and the LM head's copy of the
+ * embedding); the token-embedding table stays bf16.  Every kernel then
+ * computes with the values q * s.
+ */
+enum { HH_WF_DTYPE = 0, HH_WF_Q4G32 = 1 };
 enum { HH_LOGITS_NONE = 0, HH_LOGITS_LAST = 1, HH_LOGITS_ALL = 2 };
 
 /*
@@ -64,6 +78,8 @@ typedef struct {
   int32_t page_size;         /* KV page length in tokens; must be 16         */
   int32_t max_prefill;       /* rows per prefill pass; 0 means max_context.
                                 Longer prompts are processed in passes.      */
+  int32_t weight_format;     /* HH_WF_DTYPE or HH_WF_Q4G32 (dtype HH_BF16,
+                                d_model % 32 == 0)                           */
 } hh_config;
 
 typedef struct hh_ctx hh_ctx;
@@ -147,6 +163,20 @@ hh_status hh_stream_length(const hh_ctx* ctx, int32_t stream_id, int32_t* length
  */
 hh_status hh_read_argmax(hh_ctx* ctx, int32_t stream_id, int32_t first_pos, int32_t n,
                          int32_t* out);
+
+/*
+ * The HH_WF_Q4G32 quantizer the loader runs, on its own: quantize rows of
+ * bf16 values into the stored row format -- for each row, K / 2 bytes of
+ * codes (n = q + 8; element 2k in the low nibble of byte k, 2k + 1 in the
+ * high nibble) followed by the K / 32 scales as little-endian bf16, i.e.
+ * K / 2 + K / 16 bytes per row.
+ *  src         device, rows x K bf16 bits, row-major; finite values.
+ *  K           a positive multiple of 32.
+ *  dst         device, rows x (K / 2 + K / 16) bytes.
+ *  hip_stream  hipStream_t the kernel is enqueued on (not synchronized).
+ * Errors: INVALID_ARG (NULL pointer, rows < 1, K not a multiple of 32), HIP.
+ */
+hh_status hh_q4g32_quantize(const uint16_t* src, int64_t rows, int32_t K, uint8_t* dst, void* hip_stream);
 
 /* Destroy the host context (the arena stays the caller's). NULL is a no-op. */
 void hh_destroy(hh_ctx* ctx);

@@ -138,6 +138,10 @@ struct StepKernel {
 void widen_bf16(hipStream_t st, const __bf16* src, float* dst, size_t n);
 void absmax_bf16(hipStream_t st, const __bf16* src, size_t n, unsigned int* out_bits);
 void bf16_to_f16_scaled(hipStream_t st, const __bf16* src, _Float16* dst, size_t n, float scale);
+// 4-bit group format of rows x K bf16 values (K % 32 == 0): stored rows into
+// q4 (K / 2 + K / 16 bytes each) and/or q * s * scale as fp16 into deq
+// (either may be null; deq may equal src).
+void q4g32(hipStream_t st, const __bf16* src, size_t rows, int K, unsigned char* q4, _Float16* deq, float scale);
 // 16 x 32 operand tiles of a [rows][K] fp16 matrix taken as logical_rows rows
 // (see k_tile16); dst holds ceil(logical_rows / 16) * 16 * K elements.
 void tile16(hipStream_t st, const _Float16* src, _Float16* dst, int rows, int K, int logical_rows, int interleave_f);

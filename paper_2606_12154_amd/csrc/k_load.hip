@@ -1,6 +1,6 @@
 // Load-time weight preparation kernels: widen bf16 norm gains to fp32, find
-// the largest |w| of the bf16 matrices, and repack them to fp16 times 2^s for
-// the MFMA path.  A bf16 value v with |v| * 2^s <= 2^14 converts exactly to
+// the largest |w| of the bf16 matrices, repack them to fp16 times 2^s for
+// the MFMA path, and quantize them to the 4-bit group format.  A bf16 value v with |v| * 2^s <= 2^14 converts exactly to
 // fp16 whenever |v| * 2^s >= 2^-24 (fp16 subnormals are multiples of 2^-24 and
 // a bf16 value carries 8 significant bits), so the repack is exact for every
 // weight except magnitudes below 2^-(24 + s - 7).
@@ -92,6 +92,67 @@ __global__ void k_tile16(const _Float16* __restrict__ src, _Float16* __restrict_
 void tile16(hipStream_t st, const _Float16* src, _Float16* dst, int rows, int K, int logical_rows, int interleave_f) {
   const size_t n_chunks = (size_t)((logical_rows + 15) / 16) * 16 * K / 8;
   k_tile16<<<(unsigned)((n_chunks + 255) / 256), 256, 0, st>>>(src, dst, rows, K, interleave_f, n_chunks);
+}
+
+// The 4-bit group format: one thread per group of 32 consecutive elements of
+// a row.  Scale s = bf16(max|w| / 7), codes q = clamp(rint(w / s), -8, 7)
+// (fp32 divisions, both roundings to nearest even; s = 0 gives q = 0).  q4
+// (optional) receives the stored row: nibbles n = q + 8 (even element low),
+// then the row's scales as bf16; deq (optional) receives q * s * scale as fp16
+// -- exact, a 4-bit code times an 8-bit significand, for |q s| scale in the
+// fp16 normal range.  deq may be src (each thread reads its whole group before
+// writing it), so neither is declared restrict.
+__global__ void k_q4g32(const __bf16* src, size_t n_groups, int K, unsigned char* __restrict__ q4, _Float16* deq,
+                        float scale) {
+  const size_t gi = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (gi >= n_groups) return;
+  const int gpr = K / 32;
+  const size_t row = gi / gpr;
+  const int g = (int)(gi % gpr);
+  const size_t e0 = row * (size_t)K + 32 * (size_t)g;
+  float v[32];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const u32x4 t = *reinterpret_cast<const u32x4*>(src + e0 + 8 * c);
+    float f[8];
+    widen16(t, f, __bf16());
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[8 * c + i] = f[i];
+  }
+  float a = 0.f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) a = fmaxf(a, fabsf(v[i]));
+  const __bf16 sb = (__bf16)(a / 7.0f);
+  const float sf = (float)sb;
+  unsigned nib[4] = {0u, 0u, 0u, 0u};
+  _Float16 dq[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const float r = sf > 0.f ? v[i] / sf : 0.f;
+    const int q = min(7, max(-8, (int)rintf(r)));
+    nib[i >> 3] |= (unsigned)(q + 8) << (4 * (i & 7));
+    dq[i] = (_Float16)((float)q * sf * scale);
+  }
+  if (q4) {
+    unsigned char* rb = q4 + row * (size_t)(K / 2 + K / 16);
+    *reinterpret_cast<u32x4*>(rb + 16 * g) = u32x4{nib[0], nib[1], nib[2], nib[3]};
+    *reinterpret_cast<__bf16*>(rb + K / 2 + 2 * g) = sb;
+  }
+  if (deq) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      typedef _Float16 f16x8l __attribute__((ext_vector_type(8)));
+      f16x8l o;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = dq[8 * c + i];
+      *reinterpret_cast<f16x8l*>(deq + e0 + 8 * c) = o;
+    }
+  }
+}
+
+void q4g32(hipStream_t st, const __bf16* src, size_t rows, int K, unsigned char* q4, _Float16* deq, float scale) {
+  const size_t n = rows * (size_t)(K / 32);
+  k_q4g32<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(src, n, K, q4, deq, scale);
 }
 
 template void transpose<__bf16>(hipStream_t, const __bf16*, __bf16*, int, int);

@@ -39,6 +39,10 @@ struct Layout {
   // contexts of bf16 models only; empty otherwise).
   std::vector<size_t> wqkvT16, woT16, wguT16, wdownT16;
   size_t lm_headT16;
+  // Stored 4-bit rows (HH_WF_Q4G32 only; empty otherwise): [Wq; Wk; Wv],
+  // Wo, [Wgate; Wup], Wdown^T and the LM head, K / 2 + K / 16 bytes per row.
+  std::vector<size_t> wqkvQ, woQ, wguQ, wdownTQ;
+  size_t lm_headQ;
   size_t final_norm, rope, kv, page_table, pos, pending, slot, hist, ll, ll_words, layer_tab, trace;
   size_t row_stream, row_pos, feed, x, h, q, qM, o32, oM, m32, mM, part, logits, gemm_ws, gemm_ws_bytes, scratch_u32;
   size_t total;
@@ -63,6 +67,14 @@ bool config_supported(const hh_config& c, std::string& why) {
   if (c.d_model > 16384 || c.ffn_dim > 65536 || c.n_heads * 64 > 16384) { why = "dimension too large"; return false; }
   if (c.dtype != HH_F32 && c.dtype != HH_BF16) { why = "dtype must be HH_F32 or HH_BF16"; return false; }
   if (!(c.rms_eps >= 0.f) || !(c.rope_theta > 0.f)) { why = "bad rms_eps / rope_theta"; return false; }
+  if (c.weight_format != HH_WF_DTYPE && c.weight_format != HH_WF_Q4G32) {
+    why = "weight_format must be HH_WF_DTYPE or HH_WF_Q4G32";
+    return false;
+  }
+  if (c.weight_format == HH_WF_Q4G32 && c.dtype != HH_BF16) {
+    why = "HH_WF_Q4G32 needs bf16 weights";
+    return false;
+  }
   return true;
 }
 
@@ -116,6 +128,16 @@ Layout make_layout(const hh_config& c) {
     L.woM = L.wo;
     L.wguM = L.wgu;
     L.wdownM = L.wdown;
+  }
+  if (c.weight_format == HH_WF_Q4G32) {
+    auto q4 = [&](size_t rows, size_t K) { return take(rows * (K / 2 + K / 16)); };
+    L.lm_headQ = q4(V, d);
+    for (int l = 0; l < c.n_layers; ++l) {
+      L.wqkvQ.push_back(q4(L.nqkv, d));
+      L.woQ.push_back(q4(d, hq * 64));
+      L.wguQ.push_back(q4(2 * F, d));
+      L.wdownTQ.push_back(q4(F, d));
+    }
   }
   for (int l = 0; l < c.n_layers; ++l) {
     L.attn_norm.push_back(take(d * 4));
@@ -312,7 +334,10 @@ void enqueue_decode(hh_ctx* c, int n, bool feed, bool want_logits) {
   DK::prep_embed(c->stream, n, -1, feed ? c->at<int>(L.feed) : nullptr, c->at<int>(L.row_stream),
                  c->at<int>(L.row_pos), c->at<int>(L.pos), c->at<int>(L.pending), c->at<TW>(L.embed),
                  c->at<float>(L.x), c->cfg.d_model);
-  enqueue_layers<TW, TKV, TM>(c, n, n == 1, kSplitMax, -1, want_logits ? c->at<float>(L.logits) : nullptr);
+  // The batch-1 GEMV kernels read the model's own (bf16) matrices, which a
+  // 4-bit model does not compute with: it takes the MFMA path at one row.
+  const bool gemv = n == 1 && c->cfg.weight_format == HH_WF_DTYPE;
+  enqueue_layers<TW, TKV, TM>(c, n, gemv, kSplitMax, -1, want_logits ? c->at<float>(L.logits) : nullptr);
   finalize(c->stream, 0, n, c->at<int>(L.row_stream), c->at<int>(L.row_pos), c->at<unsigned long long>(L.slot),
            c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos), c->cfg.max_context);
 }
@@ -432,6 +457,31 @@ hh_status ensure_pages(hh_ctx* c, int s, int new_len) {
   return HH_OK;
 }
 
+// LM head + greedy key of row `row` of x into logits (optional) and the
+// row's stream slot.  A 4-bit model's head values live only in the fp16
+// copy: RMSNorm of the row, then a one-row MFMA product.
+template <typename TW, typename TKV, typename TM>
+void enqueue_head_row(hh_ctx* c, int row, float* logits, unsigned long long* slot) {
+  const Layout& L = c->L;
+  const hh_config& g = c->cfg;
+  hipStream_t st = c->stream;
+  if constexpr (sizeof(TM) == 2) {
+    if (g.weight_format == HH_WF_Q4G32) {
+      using GK = GemmKernels<TM, TKV>;
+      const GemmWorkspace gws{c->at<float>(L.gemm_ws), L.gemm_ws_bytes};
+      TM* h = c->at<TM>(L.h);
+      GK::rmsnorm(st, 1, c->at<float>(L.x) + (size_t)row * g.d_model, g.d_model, c->at<float>(L.final_norm),
+                  g.rms_eps, h);
+      GK::logits(st, gws, h, 1, c->at<TM>(L.lm_headM), g.d_model, g.vocab, 1.f / c->wscale, logits, slot,
+                 c->at<int>(L.row_stream) + row, L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16));
+      return;
+    }
+  }
+  using DK = DecodeKernels<TW, TKV, TM>;
+  DK::head_gemv(st, c->at<TW>(L.lm_head), c->at<float>(L.x), c->at<float>(L.final_norm), g.rms_eps, g.d_model,
+                g.vocab, row, c->at<int>(L.row_stream), logits, slot);
+}
+
 template <typename TW, typename TKV, typename TM>
 hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, float* logits, int32_t* next) {
   const Layout& L = c->L;
@@ -454,16 +504,12 @@ hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, f
       for (int b0 = 0; b0 < P; b0 += kLogitRows) {
         const int nb = std::min(kLogitRows, P - b0);
         for (int i = 0; i < nb; ++i)
-          DK::head_gemv(st, c->at<TW>(L.lm_head), c->at<float>(L.x), c->at<float>(L.final_norm), c->cfg.rms_eps,
-                        c->cfg.d_model, V, b0 + i, c->at<int>(L.row_stream), lbuf + (size_t)i * V,
-                        (last && b0 + i == P - 1) ? slot : nullptr);
+          enqueue_head_row<TW, TKV, TM>(c, b0 + i, lbuf + (size_t)i * V, (last && b0 + i == P - 1) ? slot : nullptr);
         HIPCHK(c, hipMemcpyAsync(logits + (size_t)(r0 + b0) * V, lbuf, (size_t)nb * V * sizeof(float),
                                  hipMemcpyDefault, st));
       }
     } else if (last) {
-      DK::head_gemv(st, c->at<TW>(L.lm_head), c->at<float>(L.x), c->at<float>(L.final_norm), c->cfg.rms_eps,
-                    c->cfg.d_model, V, P - 1, c->at<int>(L.row_stream), mode == HH_LOGITS_LAST ? lbuf : nullptr,
-                    slot);
+      enqueue_head_row<TW, TKV, TM>(c, P - 1, mode == HH_LOGITS_LAST ? lbuf : nullptr, slot);
       if (mode == HH_LOGITS_LAST)
         HIPCHK(c, hipMemcpyAsync(logits, lbuf, (size_t)V * sizeof(float), hipMemcpyDefault, st));
     }
@@ -674,12 +720,36 @@ hh_status hh_load_weights(hh_ctx* c, const void* const* tensors, int32_t n_tenso
     const int e = mx > 0.f ? (int)std::ceil(std::log2((double)mx)) : 0;
     const int sexp = std::max(-20, std::min(40, 14 - e));  // largest |w| * 2^s <= 2^14
     c->wscale = std::ldexp(1.0f, sexp);
-    for (auto& m : list)
-      bf16_to_f16_scaled(st, c->at<__bf16>(std::get<0>(m)), c->at<_Float16>(std::get<1>(m)), std::get<2>(m),
-                         c->wscale);
-    // Wdown^T of the fp16 copy, for the batch-1 decode kernel's split-K down projection.
-    for (int l = 0; l < g.n_layers; ++l)
-      transpose(st, c->at<_Float16>(L.wdownM[l]), c->at<_Float16>(L.wdownT[l]), (int)d, (int)F);
+    if (g.weight_format == HH_WF_Q4G32) {
+      // 4-bit rows for the streaming decode kernel; the fp16 copies hold their
+      // values q * s (times 2^s, exactly), so every path computes with them.
+      auto quant = [&](size_t src, size_t rows, size_t K, size_t q4, size_t dst) {
+        q4g32(st, c->at<__bf16>(src), rows, (int)K, c->at<unsigned char>(q4), c->at<_Float16>(dst), c->wscale);
+      };
+      if (g.tied_embeddings) {
+        quant(L.embed, V, d, L.lm_headQ, L.embedM);
+      } else {
+        bf16_to_f16_scaled(st, c->at<__bf16>(L.embed), c->at<_Float16>(L.embedM), V * d, c->wscale);
+        quant(L.lm_head, V, d, L.lm_headQ, L.lm_headM);
+      }
+      for (int l = 0; l < g.n_layers; ++l) {
+        quant(L.wqkv[l], L.nqkv, d, L.wqkvQ[l], L.wqkvM[l]);
+        quant(L.wo[l], d, hq * 64, L.woQ[l], L.woM[l]);
+        quant(L.wgu[l], 2 * F, d, L.wguQ[l], L.wguM[l]);
+        // W_down is grouped along its output rows: quantize the rows of its
+        // transpose (in place: bf16 in, fp16 values out), then transpose back.
+        transpose(st, c->at<__bf16>(L.wdown[l]), c->at<__bf16>(L.wdownT[l]), (int)d, (int)F);
+        quant(L.wdownT[l], F, d, L.wdownTQ[l], L.wdownT[l]);
+        transpose(st, c->at<_Float16>(L.wdownT[l]), c->at<_Float16>(L.wdownM[l]), (int)F, (int)d);
+      }
+    } else {
+      for (auto& m : list)
+        bf16_to_f16_scaled(st, c->at<__bf16>(std::get<0>(m)), c->at<_Float16>(std::get<1>(m)), std::get<2>(m),
+                           c->wscale);
+      // Wdown^T of the fp16 copy, for the batch-1 decode kernel's split-K down projection.
+      for (int l = 0; l < g.n_layers; ++l)
+        transpose(st, c->at<_Float16>(L.wdownM[l]), c->at<_Float16>(L.wdownT[l]), (int)d, (int)F);
+    }
     if (!L.wqkvT16.empty()) {
       tile16(st, c->at<_Float16>(L.lm_headM), c->at<_Float16>(L.lm_headT16), (int)V, (int)d, (int)V, 0);
       for (int l = 0; l < g.n_layers; ++l) {
@@ -802,5 +872,12 @@ void hh_destroy(hh_ctx* c) {
 }
 
 const char* hh_last_error(const hh_ctx* c) { return c ? c->err.c_str() : "NULL context"; }
+
+hh_status hh_q4g32_quantize(const uint16_t* src, int64_t rows, int32_t K, uint8_t* dst, void* hip_stream) {
+  if (!src || !dst || rows < 1 || K < 32 || K % 32 != 0) return HH_ERR_INVALID_ARG;
+  q4g32(static_cast<hipStream_t>(hip_stream), reinterpret_cast<const __bf16*>(src), (size_t)rows, K,
+        reinterpret_cast<unsigned char*>(dst), nullptr, 1.f);
+  return hipGetLastError() == hipSuccess ? HH_OK : HH_ERR_HIP;
+}
 
 }  // extern "C"

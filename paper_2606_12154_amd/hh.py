@@ -21,9 +21,11 @@ HH_OK, HH_ERR_INVALID_ARG, HH_ERR_OOM, HH_ERR_CONTEXT_FULL = 0, -1, -2, -3
 HH_ERR_NOT_LOADED, HH_ERR_HIP, HH_ERR_UNSUPPORTED = -4, -5, -6
 HH_F32, HH_BF16 = 0, 1
 HH_LOGITS_NONE, HH_LOGITS_LAST, HH_LOGITS_ALL = 0, 1, 2
+HH_WF_DTYPE, HH_WF_Q4G32 = 0, 1
 
 EXPORTED = ["hh_workspace_size", "hh_create", "hh_load_weights", "hh_prefill", "hh_decode_step",
-            "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error"]
+            "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error",
+            "hh_q4g32_quantize"]
 
 
 class hh_config(ctypes.Structure):
@@ -31,7 +33,8 @@ class hh_config(ctypes.Structure):
                                         "ffn_dim", "vocab")] + [
         ("rms_eps", c_float), ("rope_theta", c_float),
         ("tied_embeddings", c_int32), ("dtype", c_int32), ("max_streams", c_int32),
-        ("max_context", c_int32), ("page_size", c_int32), ("max_prefill", c_int32)]
+        ("max_context", c_int32), ("page_size", c_int32), ("max_prefill", c_int32),
+        ("weight_format", c_int32)]
 
 
 class HHError(RuntimeError):
@@ -63,6 +66,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hh_read_argmax": ([c_void_p, c_int32, c_int32, c_int32, i32p], c_int32),
         "hh_destroy": ([c_void_p], None),
         "hh_last_error": ([c_void_p], ctypes.c_char_p),
+        "hh_q4g32_quantize": ([c_void_p, ctypes.c_int64, c_int32, c_void_p, c_void_p], c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -130,6 +134,11 @@ def hh_last_error(ctx: int) -> str:
     return load_library().hh_last_error(ctx).decode()
 
 
+def hh_q4g32_quantize(src_ptr: int, rows: int, K: int, dst_ptr: int, hip_stream: int) -> None:
+    _check(None, load_library().hh_q4g32_quantize(c_void_p(src_ptr), rows, K, c_void_p(dst_ptr),
+                                                  c_void_p(hip_stream)))
+
+
 def _check(ctx, status: int) -> None:
     if status != HH_OK:
         raise HHError(status, hh_last_error(ctx) if ctx else "")
@@ -137,11 +146,12 @@ def _check(ctx, status: int) -> None:
 
 # ------------------------------------------------------------ convenience
 
-def make_config(shape, max_streams: int, max_context: int, max_prefill: int = 0) -> hh_config:
+def make_config(shape, max_streams: int, max_context: int, max_prefill: int = 0,
+                weight_format: int = 0) -> hh_config:
     """hh_config from a model-shape object (attributes as in synth.ModelShape)."""
     return hh_config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
                      shape.ffn_dim, shape.vocab, shape.rms_eps, shape.rope_theta, int(shape.tied),
-                     int(shape.dtype), max_streams, max_context, 16, max_prefill)
+                     int(shape.dtype), max_streams, max_context, 16, max_prefill, weight_format)
 
 
 class Context:

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions():
     text = open(os.path.join(ROOT, "include", "hh.h")).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(hh_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(hh_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_binding_names():
@@ -44,6 +44,8 @@ def test_workspace_sizes():
     ("dtype", 7, hh.HH_ERR_UNSUPPORTED),
     ("max_streams", 0, hh.HH_ERR_UNSUPPORTED),
     ("max_context", 32769, hh.HH_ERR_UNSUPPORTED),
+    ("weight_format", 2, hh.HH_ERR_UNSUPPORTED),
+    ("weight_format", hh.HH_WF_Q4G32, hh.HH_ERR_UNSUPPORTED),  # the tiny model is fp32
 ])
 def test_unsupported_configs(field, value, status):
     cfg = hh.make_config(synth.TINY, 2, 128)
@@ -69,3 +71,23 @@ def test_create_rejects_null_arena_and_small_arena():
     with pytest.raises(hh.HHError) as e:
         hh.hh_create(cfg, 1 << 20, 16, 1)
     assert e.value.status == hh.HH_ERR_OOM
+
+
+def test_q4_workspace_adds_the_stored_rows():
+    base = hh.hh_workspace_size(hh.make_config(synth.ONE_B, 1, 1024))
+    q4 = hh.hh_workspace_size(hh.make_config(synth.ONE_B, 1, 1024, weight_format=hh.HH_WF_Q4G32))
+    # 4.5 bits per weight of every streamed matrix (the head included, the
+    # embedding table not), each region rounded up to 256 bytes.
+    sh = synth.ONE_B
+    rows = sh.vocab + sh.n_layers * (sh.q_dim + 2 * sh.kv_dim + sh.d_model + 2 * sh.ffn_dim + sh.ffn_dim)
+    expect = rows * (sh.d_model // 2 + sh.d_model // 16)
+    assert expect <= q4 - base <= expect + 256 * (1 + 4 * sh.n_layers)
+
+
+def test_q4_quantize_rejects_bad_arguments():
+    with pytest.raises(hh.HHError) as e:
+        hh.hh_q4g32_quantize(1 << 20, 4, 48, 1 << 21, 0)   # K not a multiple of 32
+    assert e.value.status == hh.HH_ERR_INVALID_ARG
+    with pytest.raises(hh.HHError) as e:
+        hh.hh_q4g32_quantize(0, 4, 64, 1 << 21, 0)
+    assert e.value.status == hh.HH_ERR_INVALID_ARG

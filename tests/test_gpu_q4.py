@@ -1,0 +1,120 @@
+"""GPU parity of the 4-bit group weight format (HH_WF_Q4G32).
+
+* The quantizer (hh_q4g32_quantize, the kernel the loader runs) on seeded
+  bf16 rows -- N(0, 0.02^2) draws like the model's, plus a zero group, a group
+  whose codes land on ties (rounded to even) and a group of tiny values --
+  gives stored rows byte-identical to the oracle's (integer work: exact).
+* The 1B decoder with 4-bit weights: the oracle runs q4_model_weights of the
+  same bf16 tensors (the values q * s every GPU path computes with);
+  prompt logits (last and all rows), teacher-forced batch-1 decode, the
+  one-row MFMA decode path (HH_STEP_KERNEL=0) and four lockstep streams are
+  within max-abs 2e-2, argmax equal where the oracle's top-2 margin exceeds
+  1e-2.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import check_logits, new_context
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+def quantize_on_gpu(vals_f32):
+    import torch
+    from paper_2606_12154_amd import hh
+    R, K = vals_f32.shape
+    bits = synth.f32_to_bf16_bits(vals_f32)
+    src = torch.from_numpy(bits.view(np.int16)).to("cuda:0")
+    dst = torch.zeros(R * (K // 2 + K // 16), dtype=torch.uint8, device="cuda:0")
+    st = torch.cuda.current_stream()
+    hh.hh_q4g32_quantize(src.data_ptr(), R, K, dst.data_ptr(), st.cuda_stream)
+    torch.cuda.synchronize()
+    return dst.cpu().numpy().reshape(R, K // 2 + K // 16), synth.bf16_bits_to_f32(bits).reshape(R, K)
+
+
+def test_quantizer_bytes_match_oracle():
+    rng = np.random.default_rng(8)
+    R, K = 333, 2048
+    v = (0.02 * rng.standard_normal((R, K))).astype(np.float32)
+    v[0, :32] = 0.0                                        # zero group
+    v[1, :32] = 0.0
+    v[1, :6] = [7.0, 2.5, 3.5, -2.5, -0.5, 6.5]            # s = 1: ties to even
+    v[2, 32:64] = 1e-30 * rng.standard_normal(32)          # tiny values
+    got, exact = quantize_on_gpu(v)
+    q, s = oracle.q4_quantize_rows(exact)
+    ref = oracle.q4_pack_rows(q, s)
+    bad = np.argwhere(got != ref)
+    assert bad.size == 0, f"{len(bad)} bytes differ, first at {bad[:5].tolist()}"
+    assert q[1, :6].tolist() == [7, 2, 4, -2, 0, 6]
+
+
+@pytest.fixture(scope="module")
+def q4_model():
+    shape = synth.ONE_B
+    tensors = synth.make_weights(shape, 1)
+    w = oracle.q4_model_weights(shape, synth.weights_as_f64(shape, tensors))
+    return shape, tensors, oracle.Decoder(shape, w)
+
+
+def q4_context(shape, tensors, **kw):
+    from paper_2606_12154_amd import hh
+    ctx = hh.Context(hh.make_config(shape, kw.get("streams", 5), kw.get("context", 512), kw.get("max_prefill", 256),
+                                    weight_format=hh.HH_WF_Q4G32))
+    ctx.load_weights(tensors)
+    return ctx
+
+
+def test_q4_prefill_and_teacher_forced_decode(q4_model):
+    shape, tensors, model = q4_model
+    prompt = synth.make_tokens(shape.vocab, 256, 2)
+    ref_all, _ = model.prefill(prompt[:96])
+    ref_last, cache = model.prefill(prompt, rows="last")
+    ctx = q4_context(shape, tensors)
+    try:
+        _, got = ctx.prefill(0, prompt[:96], logits="all")
+        worst = check_logits(got, ref_all, TOL, what="q4 prefill all")
+        ctx.reset()
+        nxt, last = ctx.prefill(0, prompt, logits="last")
+        worst = max(worst, check_logits(last, ref_last[0], TOL, what="q4 prefill last"))
+        tok = int(np.argmax(ref_last[0]))
+        for i in range(24):
+            ref = model.decode(cache, tok)
+            _, lg = ctx.decode_step([0], [tok], logits=True)
+            worst = max(worst, check_logits(lg[0], ref, TOL, what=f"q4 decode step {i}"))
+            tok = int(np.argmax(ref))
+        print(f"1B 4-bit prefill + teacher-forced decode: max-abs {worst:.4g}")
+    finally:
+        ctx.close()
+
+
+def test_q4_one_row_mfma_path_and_streams(q4_model):
+    shape, tensors, model = q4_model
+    os.environ["HH_STEP_KERNEL"] = "0"
+    try:
+        ctx = q4_context(shape, tensors)
+    finally:
+        del os.environ["HH_STEP_KERNEL"]
+    try:
+        lens = [16, 33, 7, 48]
+        prompts = [synth.make_tokens(shape.vocab, n, 100 + i) for i, n in enumerate(lens)]
+        caches = []
+        for i, p in enumerate(prompts):
+            ctx.prefill(i, p)
+            caches.append(model.prefill(p, rows="last")[1])
+        rng = np.random.default_rng(11)
+        worst = 0.0
+        for step in range(2):
+            feed = rng.integers(0, shape.vocab, size=4).astype(np.int32)
+            _, lg = ctx.decode_step([0, 1, 2, 3], feed, logits=True)
+            worst = max(worst, check_logits(lg, model.decode_batch(caches, feed), TOL, what=f"q4 4 streams {step}"))
+        t = int(rng.integers(0, shape.vocab))
+        _, lg = ctx.decode_step([2], [t], logits=True)   # one row, no persistent kernel
+        worst = max(worst, check_logits(lg[0], model.decode(caches[2], t), TOL, what="q4 one-row MFMA"))
+        print(f"1B 4-bit multi-stream and one-row paths: max-abs {worst:.4g}")
+    finally:
+        ctx.close()
