@@ -160,6 +160,57 @@ def measure_others(ctx, shape, st, names):
     return other
 
 
+def q4_step_bytes(shape, t: float) -> float:
+    """Algorithmic HBM bytes of one batch-1 decode launch of the 4-bit model:
+    every streamed matrix's stored rows (K / 2 bytes of codes + K / 16 of
+    bf16 scales per row of K = d_model), the K/V of t positions, the new
+    position's K/V write and the embedding row read."""
+    d = shape.d_model
+    rows = shape.vocab + shape.n_layers * (shape.q_dim + 2 * shape.kv_dim + d + 3 * shape.ffn_dim)
+    return rows * (d // 2 + d // 16) + kv_bytes_per_position(shape) * (t + 1) + 2 * d
+
+
+def measure_q4_decode(shape):
+    """The bench workload (256-token prompt, 256 device-fed greedy steps) on
+    the 4-bit model (HH_WF_Q4G32, quantized at load from the same seeded
+    bf16 weights): TTFT and decode rate, and the HBM fraction of the
+    4-bit stream."""
+    import torch
+
+    import synth
+    from paper_2606_12154_amd import hh
+    wl = synth.WORKLOADS["1b_decode"]
+    P, N = wl["prompt"], wl["steps"]
+    tensors = synth.make_weights(shape, wl["wseed"])
+    ctx = hh.Context(hh.make_config(shape, 1, P + N + 8, P, weight_format=hh.HH_WF_Q4G32))
+    ctx.load_weights(tensors)
+    del tensors
+    st = ctx.stream
+    prompt = synth.make_tokens(shape.vocab, P, wl["tseed"])
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    tt, ms = [], []
+    for rep in range(4):
+        ctx.reset(0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ctx.prefill(0, prompt)
+        tt.append(time.perf_counter() - t0)
+        e0.record(st)
+        for _ in range(N):
+            hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+        e1.record(st)
+        e1.synchronize()
+        ms.append(e0.elapsed_time(e1) / N)
+    ctx.close()
+    tt, ms = tt[1:], ms[1:]
+    sec = float(np.mean(ms)) / 1e3
+    b = q4_step_bytes(shape, P + (N - 1) / 2.0 + 1)
+    return {"decode_tok_s": round(1.0 / sec, 1), "ms_per_token": round(sec * 1e3, 4),
+            "ttft_ms": round(float(np.mean(tt)) * 1e3, 3), "bytes_per_token": int(b),
+            "hbm_frac": round(b / sec / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def measure_ctx_sweep(shape):
     """Decode rate against the number of cached positions (the paper's window
     sweep, here over positions actually attended): a 1-stream context of
@@ -206,7 +257,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--other-configs", action="store_true",
                     help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
-    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep"],
+    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep", "q4decode"],
                     help="measure just this one of the other workloads (for a kernel trace of it); "
                          "prints its figures instead of the decode line")
     ap.add_argument("--cpu-decode-steps", type=int, default=8)
@@ -225,6 +276,10 @@ def main():
 
     wl = synth.WORKLOADS["1b_decode"]
     shape, P, N = wl["shape"], wl["prompt"], wl["steps"]
+    if args.only == "q4decode":
+        print(json.dumps({"metric": METRIC, "workload": "q4decode", "data": "synthetic", "n_gpus": 1,
+                          **measure_q4_decode(shape)}), flush=True)
+        return
     if args.only == "ctxsweep":
         rows = measure_ctx_sweep(shape)
         print(json.dumps({"metric": METRIC, "workload": "ctxsweep", "data": "synthetic", "n_gpus": 1,

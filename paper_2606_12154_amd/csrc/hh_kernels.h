@@ -87,6 +87,11 @@ struct LayerPtrs {
 // looks up stays in the model's own type.
 template <typename TW> struct StepEmbed { using type = TW; };
 template <> struct StepEmbed<_Float16> { using type = __bf16; };
+// Element tag of the 4-bit rows (HH_WF_Q4G32, d_model 2048: 1024 bytes of
+// codes and 64 bf16 scales per row) the batch-1 kernel streams for 4-bit
+// models; their embedding table stays bf16.
+struct Q4Row {};
+template <> struct StepEmbed<Q4Row> { using type = __bf16; };
 
 template <typename TW, typename TKV>
 struct StepParams {

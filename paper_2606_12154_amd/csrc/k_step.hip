@@ -43,6 +43,8 @@
 // workgroup.
 #include "hh_kernels.h"
 
+#include <type_traits>
+
 namespace hh {
 
 constexpr int kWaves = kStepThreads / 64;  // 8
@@ -52,6 +54,16 @@ constexpr int kNC = kWaves - kLoaders;     // compute waves
 constexpr int kPollX = (2048 + 64 * kNC - 1) / (64 * kNC);
 constexpr int kHeadsPerWave = (32 + kNC - 1) / kNC;
 constexpr int kSlot = 8192;                // ring slot: 8 pieces of 1 KiB
+// 4-bit rows (d = 2048): 1024 bytes of codes + 64 bf16 scales.  A slot holds
+// seven: codes of row r at 1024 r, all scales from kQ4ScaleOff (128 B a row).
+constexpr int kQ4Rows = 7;
+constexpr int kQ4RowBytes = 1152;
+constexpr int kQ4ScaleOff = kQ4Rows * 1024;
+
+// Rows per 4-bit slot for a segment of n rows: short segments (the q/k/v and
+// O rows of one workgroup) are cut into thinner slots so that every compute
+// wave gets some; the three sizes are the compiled variants of the row code.
+__host__ __device__ constexpr int q4_rows(int n) { return n <= 2 * kNC ? 2 : n <= 3 * kNC ? 3 : kQ4Rows; }
 constexpr int kMaxRing = 16;               // ring slots supported
 constexpr int kItemKvBytes = 64 * 1024;    // K/V bytes aimed at per attention item
 constexpr int kMaxItemPages = 256;         // pages of one attention item
@@ -411,8 +423,10 @@ __device__ __forceinline__ void make_plan(Plan& pl, const StepParams<TW, TKV>& P
   // SwiGLU outputs: item workgroups take fewer, so every workgroup streams
   // about the same bytes per layer.  An output is three d-rows (gate, up,
   // and the Wdown^T row it multiplies).
+  constexpr bool q4 = std::is_same<TW, Q4Row>::value;
   const int kv_slots = (per + pps - 1) / pps;
-  const int gu_unit = 3 * NPD * 1024;  // bytes of one output's rows: gate, up and its Wdown^T row
+  // Bytes of one output's rows: gate, up and its Wdown^T row.
+  const int gu_unit = 3 * (q4 ? kQ4RowBytes : NPD * 1024);
   int kvu = (kv_slots * kSlot + gu_unit / 2) / gu_unit;
   long long tot = (long long)F + (long long)pl.n_items * kvu;
   if (tot < (long long)kvu * nwg) {  // items would get a negative share: plain split
@@ -425,18 +439,19 @@ __device__ __forceinline__ void make_plan(Plan& pl, const StepParams<TW, TKV>& P
   };
   pl.j0 = cum(wg);
   pl.j1 = cum(wg + 1);
-  pl.n_qkv = row_slots(2 * (pl.pq1 - pl.pq0), NPD);
+  auto slots = [&](int n) { return q4 ? (n + q4_rows(n) - 1) / q4_rows(n) : row_slots(n, NPD); };
+  pl.n_qkv = slots(2 * (pl.pq1 - pl.pq0));
   pl.n_kv = pl.has_item ? (pl.it_pg1 - pl.it_pg0 + pps - 1) / pps : 0;
-  pl.n_o = row_slots(pl.rd1 - pl.rd0, NPD);
-  pl.n_gu = row_slots(2 * (pl.j1 - pl.j0), NPD);
-  pl.n_down = row_slots(pl.j1 - pl.j0, NPD);
+  pl.n_o = slots(pl.rd1 - pl.rd0);
+  pl.n_gu = slots(2 * (pl.j1 - pl.j0));
+  pl.n_down = slots(pl.j1 - pl.j0);
   pl.o_qkv = 0;
   pl.o_kv = pl.n_qkv;
   pl.o_o = pl.o_kv + pl.n_kv;
   pl.o_gu = pl.o_o + pl.n_o;
   pl.o_down = pl.o_gu + pl.n_gu;
   pl.per_layer = pl.o_down + pl.n_down;
-  pl.head_slots = row_slots(pl.v1 - pl.v0, NPD);
+  pl.head_slots = slots(pl.v1 - pl.v0);
 }
 
 // ---------------------------------------------------------------- streaming
@@ -477,6 +492,126 @@ __device__ __forceinline__ void issue_row_slot(char* dst, const char* W, const R
       __builtin_amdgcn_global_load_lds(src + off, dst + q * 1024, 16, 0, 2);
     }
   }
+}
+
+// The 8 direct global->LDS loads of a slot of 4-bit rows: up to seven rows'
+// codes (lane l: 16 bytes at 16 l), then their scales (lane l < 56: bytes
+// 16 (l % 8) .. + 16 of row l / 8's scales).  The slot holds rows R k ..
+// R k + R - 1 of the segment (R = q4_rows(nrows)); its other row places, and
+// rows missing at the end of the segment, repeat the slot's first row, so
+// every slot costs the same 8 loads.
+__device__ __forceinline__ void issue_q4_slot(char* dst, const char* W, const RowMap& map, int nrows, int k) {
+  const int lane = threadIdx.x & 63;
+  const int R = q4_rows(nrows);
+  const int lr0 = k * R;
+  const char* first = W + (size_t)map(lr0) * kQ4RowBytes;
+  auto row_ptr = [&](int r) {
+    return r == 0 ? first : r < R && lr0 + r < nrows ? W + (size_t)map(lr0 + r) * kQ4RowBytes : first;
+  };
+#pragma unroll
+  for (int r = 0; r < kQ4Rows; ++r) __builtin_amdgcn_global_load_lds(row_ptr(r) + lane * 16, dst + r * 1024, 16, 0, 2);
+  const int rs = lane >> 3;
+  const char* srow = row_ptr(rs < kQ4Rows ? rs : 0);
+  if (lane < 8 * kQ4Rows) __builtin_amdgcn_global_load_lds(srow + 1024 + (lane & 7) * 16, dst + kQ4ScaleOff, 16, 0, 2);
+}
+
+typedef _Float16 h2x __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ unsigned and_or(unsigned a, unsigned m, unsigned o) {
+  unsigned r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "s"(m), "v"(o));
+  return r;
+}
+
+// A code word (byte b: element 2 b in the low nibble, 2 b + 1 in the high
+// one) as four fp16 pairs, pair j holding elements j and j + 4.  A nibble n
+// placed in the low mantissa bits of 1024 reads 1024 + n, one nibble up
+// 1024 + 16 n (pairs 1 and 3).  q4_biased returns these raw pairs; q4_codes
+// turns them into q = n - 8 exactly (a subtraction, or a fused scale and
+// subtraction).
+__device__ __forceinline__ void q4_biased(unsigned wd, unsigned* p) {
+  const unsigned mg = 0x64006400u, w8 = wd >> 8;
+  p[0] = and_or(wd, 0x000F000Fu, mg);
+  p[1] = and_or(wd, 0x00F000F0u, mg);
+  p[2] = and_or(w8, 0x000F000Fu, mg);
+  p[3] = and_or(w8, 0x00F000F0u, mg);
+}
+__device__ __forceinline__ void q4_codes(unsigned wd, h2x* q) {
+  unsigned p[4];
+  q4_biased(wd, p);
+  const h2x c0 = {(_Float16)-1032.f, (_Float16)-1032.f};
+  const h2x sc = {(_Float16)0.0625f, (_Float16)0.0625f}, c1 = {(_Float16)-72.f, (_Float16)-72.f};
+  q[0] = __builtin_bit_cast(h2x, p[0]) + c0;
+  q[1] = __builtin_elementwise_fma(__builtin_bit_cast(h2x, p[1]), sc, c1);
+  q[2] = __builtin_bit_cast(h2x, p[2]) + c0;
+  q[3] = __builtin_elementwise_fma(__builtin_bit_cast(h2x, p[3]), sc, c1);
+}
+
+// R 4-bit rows of one slot against the staged input.  Lane l takes, as the
+// 16-bit rows do, elements 512 c + 8 l .. + 8 (c < 4): code word c is the 4
+// bytes at 256 c + 4 l of the row's codes (consecutive lanes, consecutive
+// words) and its group is 16 c + l / 4.  The input comes in the layout of
+// the biased code pairs: xh[4 c + j] holds the lane's inputs j and j + 4 of
+// chunk c in fp16, divided by 16 for j = 1, 3, and xb[c] = -(1032 (sum of
+// the j = 0, 2 halves) + 1152 (sum of the j = 1, 3 halves)), so that four
+// 2-term dot products started from xb[c] give sum x q for the word, which
+// its group's scale multiplies.  Row totals: a transposed reduction (lane
+// swaps across the wave halves and 16-lane rows, then DPP within 8 lanes)
+// leaves row bitrev3(l / 8) in lanes l.
+template <int R>
+__device__ __forceinline__ void q4_slot_rows(const char* slot, const h2x* xh, const float* xb, int k, int n_rows,
+                                             float* res) {
+  static_assert(R >= 1 && R <= kQ4Rows, "rows per slot");
+  const int lane = threadIdx.x & 63;
+  // All of the slot's words and scales are read before any is used, so the
+  // LDS reads overlap instead of each waiting for the one before.
+  unsigned wds[R][4];
+  float scs[R][4];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      wds[r][c] = *reinterpret_cast<const unsigned*>(slot + r * 1024 + 256 * c + 4 * lane);
+      scs[r][c] = (float)*reinterpret_cast<const __bf16*>(slot + kQ4ScaleOff + r * 128 + 2 * (16 * c + (lane >> 2)));
+    }
+  float v[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) v[r] = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      unsigned p[4];
+      q4_biased(wds[r][c], p);
+      float t = xb[c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) t = __builtin_amdgcn_fdot2(xh[4 * c + j], __builtin_bit_cast(h2x, p[j]), t, false);
+      v[r] = fmaf(t, scs[r][c], v[r]);
+    }
+  // Rows (2 i, 2 i + 1) -> wave halves, then pairs of those -> 16-lane rows:
+  // w[0] holds rows 0, 2, 1, 3 and w[1] rows 4, 6, 5, 7 in lane rows 0..3.
+  float u[4], w[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[2 * i]), __float_as_uint(v[2 * i + 1]), false,
+                                                     false);
+    u[i] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(u[2 * i]), __float_as_uint(u[2 * i + 1]), false,
+                                                     false);
+    w[i] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  }
+  // Halves of each 16-lane row: w[0] stays in lanes 0..7, w[1] in 8..15.
+  const bool hi8 = (lane & 8) != 0;
+  float tot = (hi8 ? w[1] : w[0]) + dpp<0x128>(hi8 ? w[0] : w[1]);
+  tot += dpp<0xB1>(tot);   // lane ^ 1
+  tot += dpp<0x4E>(tot);   // lane ^ 2
+  tot += dpp<0x141>(tot);  // mirror within 8 lanes
+  const int g = lane >> 3;
+  const int r = ((g & 1) << 2) | (g & 2) | (g >> 2);
+  if ((lane & 7) == 0 && r < R && k * R + r < n_rows) res[k * R + r] = tot;
 }
 
 // ---------------------------------------------------------------- kernel
@@ -583,7 +718,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
         RowMap map{0, 0, 0, F};
         int nrows = 0, rowb = 0;
         if (sg != SG_KV) {
-          rowb = d * (int)sizeof(TW);
+          rowb = std::is_same<TW, Q4Row>::value ? kQ4RowBytes : d * (int)sizeof(TW);
           if (sg == SG_QKV) {
             W = reinterpret_cast<const char*>(lptr[l].wqkv);
             map = RowMap{1, pl.pq0, 0, F};
@@ -669,6 +804,8 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
               }
               __builtin_amdgcn_global_load_lds(src, dst + q * 1024, 16, 0, 0);
             }
+          } else if constexpr (std::is_same<TW, Q4Row>::value) {
+            issue_q4_slot(dst, W, map, nrows, k);
           } else {
             issue_row_slot<NPD>(dst, W, map, rowb, nrows, k, full);
           }
@@ -765,11 +902,44 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
 
   // Consume this wave's slots of a row segment (global slot index base);
   auto run_rows = [&](int base, int nsl, const float* xs, int K, int nrows) {
-    for (int k = cw; k < nsl; k += kNC) {
-      const int n = base + k, pos = n % S;
-      wait_landed(syp, n, pos, err);
-      slot_rows<TW, NPD, FD>(ring + (size_t)pos * kSlot, xs, K, k, nrows, res);
-      release_slot(syp, pos, n);
+    if constexpr (std::is_same<TW, Q4Row>::value) {
+      // This lane's 32 inputs (elements 512 c + 8 l + e) in the layout of the
+      // biased code pairs serve every slot of the phase.
+      h2x xh[16];
+      float xb[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float4 a = *reinterpret_cast<const float4*>(xs + 512 * c + 8 * lane);
+        const float4 b = *reinterpret_cast<const float4*>(xs + 512 * c + 8 * lane + 4);
+        xh[4 * c] = h2x{(_Float16)a.x, (_Float16)b.x};
+        xh[4 * c + 1] = h2x{(_Float16)(a.y * 0.0625f), (_Float16)(b.y * 0.0625f)};
+        xh[4 * c + 2] = h2x{(_Float16)a.z, (_Float16)b.z};
+        xh[4 * c + 3] = h2x{(_Float16)(a.w * 0.0625f), (_Float16)(b.w * 0.0625f)};
+        const float s02 = ((float)xh[4 * c].x + (float)xh[4 * c].y) + ((float)xh[4 * c + 2].x + (float)xh[4 * c + 2].y);
+        const float s13 =
+            ((float)xh[4 * c + 1].x + (float)xh[4 * c + 1].y) + ((float)xh[4 * c + 3].x + (float)xh[4 * c + 3].y);
+        xb[c] = -fmaf(1032.f, s02, 1152.f * s13);
+      }
+      auto rows = [&](auto RC) {
+        constexpr int R = decltype(RC)::value;
+        for (int k = cw; k < nsl; k += kNC) {
+          const int n = base + k, pos = n % S;
+          wait_landed(syp, n, pos, err);
+          q4_slot_rows<R>(ring + (size_t)pos * kSlot, xh, xb, k, nrows, res);
+          release_slot(syp, pos, n);
+        }
+      };
+      const int R = q4_rows(nrows);
+      if (R == 2) rows(std::integral_constant<int, 2>{});
+      else if (R == 3) rows(std::integral_constant<int, 3>{});
+      else rows(std::integral_constant<int, kQ4Rows>{});
+    } else {
+      for (int k = cw; k < nsl; k += kNC) {
+        const int n = base + k, pos = n % S;
+        wait_landed(syp, n, pos, err);
+        slot_rows<TW, NPD, FD>(ring + (size_t)pos * kSlot, xs, K, k, nrows, res);
+        release_slot(syp, pos, n);
+      }
     }
   };
 
@@ -1210,40 +1380,99 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
     // output, no exchange of the SwiGLU vector.  Partials are summed per
     // output row, in workgroup order, by the row's owner.
     {
-      constexpr int E = 16 / (int)sizeof(TW), PE = 1024 / (int)sizeof(TW);
-      constexpr int RPS = rows_per_slot(NPD);
-      float acc[NPD * E];
-#pragma unroll
-      for (int i = 0; i < NPD * E; ++i) acc[i] = 0.f;
+      float* red = xa;  // [kNC][d] over the staging buffers, idle once the slots are done
       const int dbase = lbase + pl.o_down;
-      for (int k = cw; k < pl.n_down; k += kNC) {
-        const int n = dbase + k, pos = n % S;
-        wait_landed(syp, n, pos, err);
-        const char* slot = ring + (size_t)pos * kSlot;
+      if constexpr (std::is_same<TW, Q4Row>::value) {
+        // 4-bit Wdown^T rows: lane l accumulates outputs 512 c + 8 l + e (as
+        // the 16-bit rows do): sum_j c_j q_je with c_j = m_j s_j,(16c + l/4).
+        float acc[32];
 #pragma unroll
-        for (int r = 0; r < RPS; ++r) {
-          const int jl = k * RPS + r;
-          // Rows missing from the slot repeat its first row: weight 0.
-          const float mj = jl < nj ? silu(res[jl] * (inv * ws)) * (res[nj + jl] * (inv * ws)) : 0.f;
+        for (int i = 0; i < 32; ++i) acc[i] = 0.f;
+        auto rows = [&](auto RC) {
+          constexpr int R = decltype(RC)::value;
+          for (int k = cw; k < pl.n_down; k += kNC) {
+            const int n = dbase + k, pos = n % S;
+            wait_landed(syp, n, pos, err);
+            const char* slot = ring + (size_t)pos * kSlot;
+            // Words and scales first (the LDS reads overlap), then the FMAs.
+            unsigned wds[R][4];
+            float scs[R][4];
 #pragma unroll
-          for (int c = 0; c < NPD; ++c) {
-            const u32x4 w = *reinterpret_cast<const u32x4*>(slot + (r * NPD + c) * 1024 + lane * 16);
-            float wf[E];
-            widen16(w, wf, TW());
+            for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int e = 0; e < E; ++e) acc[c * E + e] = fmaf(mj, wf[e], acc[c * E + e]);
+              for (int c = 0; c < 4; ++c) {
+                wds[r][c] = *reinterpret_cast<const unsigned*>(slot + r * 1024 + 256 * c + 4 * lane);
+                scs[r][c] = (float)*reinterpret_cast<const __bf16*>(slot + kQ4ScaleOff + r * 128 +
+                                                                     2 * (16 * c + (lane >> 2)));
+              }
+            // Lane r < R forms the SwiGLU output of the slot's row r (rows
+            // missing from the slot repeat its first row: weight 0).
+            const int jv = k * R + lane;
+            const float mv =
+                lane < R && jv < nj ? silu(res[jv] * (inv * ws)) * (res[nj + jv] * (inv * ws)) : 0.f;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+              const float mj = lane_read(mv, r);
+#pragma unroll
+              for (int c = 0; c < 4; ++c) {
+                const float cj = mj * scs[r][c];
+                h2x q[4];
+                q4_codes(wds[r][c], q);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                  acc[8 * c + j] = fmaf(cj, (float)q[j].x, acc[8 * c + j]);
+                  acc[8 * c + j + 4] = fmaf(cj, (float)q[j].y, acc[8 * c + j + 4]);
+                }
+              }
+            }
+            release_slot(syp, pos, n);
           }
+        };
+        const int R = q4_rows(nj);
+        if (R == 2) rows(std::integral_constant<int, 2>{});
+        else if (R == 3) rows(std::integral_constant<int, 3>{});
+        else rows(std::integral_constant<int, kQ4Rows>{});
+        // Sum the compute waves' partials (fixed order) and publish them.
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int e = 0; e < 8; e += 4)
+            *reinterpret_cast<float4*>(red + (size_t)cw * d + 512 * c + 8 * lane + e) =
+                make_float4(acc[8 * c + e], acc[8 * c + e + 1], acc[8 * c + e + 2], acc[8 * c + e + 3]);
+      } else {
+        constexpr int E = 16 / (int)sizeof(TW), PE = 1024 / (int)sizeof(TW);
+        constexpr int RPS = rows_per_slot(NPD);
+        float acc[NPD * E];
+#pragma unroll
+        for (int i = 0; i < NPD * E; ++i) acc[i] = 0.f;
+        for (int k = cw; k < pl.n_down; k += kNC) {
+          const int n = dbase + k, pos = n % S;
+          wait_landed(syp, n, pos, err);
+          const char* slot = ring + (size_t)pos * kSlot;
+#pragma unroll
+          for (int r = 0; r < RPS; ++r) {
+            const int jl = k * RPS + r;
+            // Rows missing from the slot repeat its first row: weight 0.
+            const float mj = jl < nj ? silu(res[jl] * (inv * ws)) * (res[nj + jl] * (inv * ws)) : 0.f;
+#pragma unroll
+            for (int c = 0; c < NPD; ++c) {
+              const u32x4 w = *reinterpret_cast<const u32x4*>(slot + (r * NPD + c) * 1024 + lane * 16);
+              float wf[E];
+              widen16(w, wf, TW());
+#pragma unroll
+              for (int e = 0; e < E; ++e) acc[c * E + e] = fmaf(mj, wf[e], acc[c * E + e]);
+            }
+          }
+          release_slot(syp, pos, n);
         }
-        release_slot(syp, pos, n);
+        // Sum the compute waves' partials (fixed order) and publish them.
+#pragma unroll
+        for (int c = 0; c < NPD; ++c)
+#pragma unroll
+          for (int e = 0; e < E; e += 4)
+            *reinterpret_cast<float4*>(red + (size_t)cw * d + c * PE + lane * E + e) =
+                make_float4(acc[c * E + e], acc[c * E + e + 1], acc[c * E + e + 2], acc[c * E + e + 3]);
       }
-      // Sum the compute waves' partials (fixed order) and publish them.
-      float* red = xa;  // [kNC][d] over the staging buffers, idle now
-#pragma unroll
-      for (int c = 0; c < NPD; ++c)
-#pragma unroll
-        for (int e = 0; e < E; e += 4)
-          *reinterpret_cast<float4*>(red + (size_t)cw * d + c * PE + lane * E + e) =
-              make_float4(acc[c * E + e], acc[c * E + e + 1], acc[c * E + e + 2], acc[c * E + e + 3]);
       cbar(syp, gen, err);
       STEP_MARK(l, 15);
       {
@@ -1388,10 +1617,12 @@ static hipError_t launch_step(const StepParams<TW, TKV>& P, int nwg, hipStream_t
 }
 
 // Instantiated row shapes (every streamed row has d elements): bf16 rows of
-// exactly 4 pieces (d = 2048), fp32 rows of exactly 1 piece (d = 256).
+// exactly 4 pieces (d = 2048), fp32 rows of exactly 1 piece (d = 256), 4-bit
+// rows of 1152 bytes (d = 2048; their slots are laid out separately).
 template <typename TW>
 static bool shape_ok(int d, int F) {
   (void)F;
+  if constexpr (std::is_same<TW, Q4Row>::value) return d == 2048;  // 64 groups: one per lane
   if (sizeof(TW) == 2) return d * 2 == 4 * 1024;
   return d * 4 == 1024;
 }
@@ -1431,5 +1662,6 @@ int StepKernel<TW, TKV>::max_blocks_per_cu(int d, int F, int hq, int hkv) {
 
 template struct StepKernel<_Float16, _Float16>;
 template struct StepKernel<float, float>;
+template struct StepKernel<Q4Row, _Float16>;
 
 }  // namespace hh

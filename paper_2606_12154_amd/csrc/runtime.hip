@@ -13,6 +13,7 @@
 #include <map>
 #include <string>
 #include <tuple>
+#include <type_traits>
 #include <vector>
 
 #include "hh.h"
@@ -202,6 +203,7 @@ struct hh_ctx {
   bool use_graphs = true;
   float wscale = 1.f;  // MFMA weights hold w * wscale (fp16 repack); epilogues multiply by 1/wscale
   int step_wg = 0;     // workgroups of the persistent batch-1 decode kernel (0: not usable)
+  bool step_q4 = false;  // the persistent kernel streams the stored 4-bit rows
   unsigned step_count = 0;  // persistent-kernel launches so far (names each step's epochs)
   int step_depth = kStepLoadDepth;  // HH_LOAD_DEPTH: ring slots in flight per streaming wave
   int step_quiet = 0;               // HH_STEP_QUIET: pause streaming during exchange waits
@@ -377,8 +379,33 @@ int step_workgroups(const hh_config& g) {
   return nwg;
 }
 
+// 4-bit models: the stored rows of every streamed matrix (Wdown^T for the
+// split-K down projection; the unused Wdown slot repeats it).
+hipError_t setup_step_tables_q4(hh_ctx* c) {
+  const hh_config& g = c->cfg;
+  const Layout& L = c->L;
+  std::vector<LayerPtrs<Q4Row>> tab(g.n_layers);
+  for (int l = 0; l < g.n_layers; ++l)
+    tab[l] = LayerPtrs<Q4Row>{c->at<Q4Row>(L.wqkvQ[l]),   c->at<Q4Row>(L.woQ[l]),
+                              c->at<Q4Row>(L.wguQ[l]),    c->at<Q4Row>(L.wdownTQ[l]),
+                              c->at<Q4Row>(L.wdownTQ[l]), c->at<float>(L.attn_norm[l]),
+                              c->at<float>(L.mlp_norm[l])};
+  if (g.n_layers == 0) return hipSuccess;
+  hipError_t e = hipMemcpyAsync(c->arena + L.layer_tab, tab.data(), tab.size() * sizeof(LayerPtrs<Q4Row>),
+                                hipMemcpyHostToDevice, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  return e;
+}
+
 hipError_t setup_step_kernel(hh_ctx* c) {
   if (c->cfg.dtype == HH_BF16) {
+    if (c->cfg.weight_format == HH_WF_Q4G32) {
+      // Without the 4-bit kernel (other shapes) the fp16 one streams the
+      // fp16 copies, which hold the same values.
+      c->step_wg = step_workgroups<Q4Row, _Float16>(c->cfg);
+      c->step_q4 = c->step_wg > 0;
+      if (c->step_q4) return setup_step_tables_q4(c);
+    }
     c->step_wg = step_workgroups<_Float16, _Float16>(c->cfg);
     return setup_step_tables<_Float16>(c);
   }
@@ -410,8 +437,10 @@ hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
   P.epoch = c->step_count * 512u;
   P.layer = c->at<LayerPtrs<TW>>(L.layer_tab);
   P.embed = c->at<typename StepEmbed<TW>::type>(L.embed);
-  P.head = c->at<TW>(L.lm_headM);
-  P.wscale_inv = 1.0f / c->wscale;
+  // 4-bit rows carry their own scales (no power-of-two factor).
+  constexpr bool q4 = std::is_same<TW, Q4Row>::value;
+  P.head = c->at<TW>(q4 ? L.lm_headQ : L.lm_headM);
+  P.wscale_inv = q4 ? 1.0f : 1.0f / c->wscale;
   P.final_norm = c->at<float>(L.final_norm);
   P.rope = c->at<float2>(L.rope);
   P.kvc = c->at<TKV>(L.kv);
@@ -538,7 +567,12 @@ hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t
   if (tokens) HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, n * sizeof(int), hipMemcpyHostToDevice, st));
   const bool want_logits = logits != nullptr;
   if (n == 1 && c->step_wg > 0) {
-    hh_status rc = launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits);
+    hh_status rc;
+    if constexpr (sizeof(TM) == 2)
+      rc = c->step_q4 ? launch_step<Q4Row, TKV>(c, ids[0], tokens != nullptr, want_logits)
+                      : launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits);
+    else
+      rc = launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits);
     if (rc != HH_OK) return rc;
   } else if (c->use_graphs) {
     auto key = std::make_tuple(n, tokens != nullptr ? 1 : 0, want_logits ? 1 : 0);
