@@ -214,7 +214,7 @@ def measure_q4_decode(shape):
 def measure_ctx_sweep(shape):
     """Decode rate against the number of cached positions (the paper's window
     sweep, here over positions actually attended): a 1-stream context of
-    32768 positions; for each length a seeded prompt fills the cache
+    131072 positions; for each length a seeded prompt fills the cache
     (untimed), then 64 device-fed decode steps are timed."""
     import torch
 
@@ -222,14 +222,14 @@ def measure_ctx_sweep(shape):
     from paper_2606_12154_amd import hh
     steps = 64
     tensors = synth.make_weights(shape, synth.WORKLOADS["1b_decode"]["wseed"])
-    ctx = hh.Context(hh.make_config(shape, 1, 32768, 8192))
+    ctx = hh.Context(hh.make_config(shape, 1, 131072, 8192))
     ctx.load_weights(tensors)
     del tensors
     st = ctx.stream
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     rows = []
-    for n in (1024, 2048, 4096, 8192, 16384, 32768 - steps):
+    for n in (1024, 2048, 4096, 8192, 16384, 32768, 65536, 131072 - steps):
         ctx.reset(0)
         ctx.prefill(0, synth.make_tokens(shape.vocab, n, 500 + n))
         hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
@@ -249,6 +249,50 @@ def measure_ctx_sweep(shape):
     return rows
 
 
+def measure_windows(shape):
+    """The paper's window sweep as stated (allocated context, short use): for
+    windows of 4K..128K positions, the arena the library asks for and the
+    decode rate of the bench request (256-token prompt, 256 device-fed
+    steps) in a context of that window.  The bf16 weights are uploaded once
+    and loaded from device memory into each context."""
+    import torch
+
+    import synth
+    from paper_2606_12154_amd import hh
+    wl = synth.WORKLOADS["1b_decode"]
+    P, N = wl["prompt"], wl["steps"]
+    tensors = [torch.from_numpy(np.ascontiguousarray(t).view(np.int16) if t.dtype == np.uint16 else np.ascontiguousarray(t))
+               for t in synth.make_weights(shape, wl["wseed"])]
+    dev = [t.to("cuda") for t in tensors]
+    del tensors
+    prompt = synth.make_tokens(shape.vocab, P, wl["tseed"])
+    rows = []
+    for w in (4096, 8192, 16384, 32768, 65536, 131072):
+        cfg = hh.make_config(shape, 1, w, P)
+        ctx = hh.Context(cfg)
+        ctx.load_weights(dev)
+        st = ctx.stream
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        ms = []
+        for rep in range(3):
+            ctx.reset(0)
+            ctx.prefill(0, prompt)
+            e0.record(st)
+            for _ in range(N):
+                hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
+            e1.record(st)
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1) / N)
+        ctx.close()
+        del ctx
+        sec = float(np.mean(ms[1:])) / 1e3
+        rows.append({"window": w, "arena_bytes": int(hh.hh_workspace_size(cfg)),
+                     "decode_tok_s": round(1.0 / sec, 1), "ms_per_token": round(sec * 1e3, 4)})
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -257,7 +301,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--other-configs", action="store_true",
                     help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
-    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep", "q4decode"],
+    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep", "windows", "q4decode"],
                     help="measure just this one of the other workloads (for a kernel trace of it); "
                          "prints its figures instead of the decode line")
     ap.add_argument("--cpu-decode-steps", type=int, default=8)
@@ -279,6 +323,11 @@ def main():
     if args.only == "q4decode":
         print(json.dumps({"metric": METRIC, "workload": "q4decode", "data": "synthetic", "n_gpus": 1,
                           **measure_q4_decode(shape)}), flush=True)
+        return
+    if args.only == "windows":
+        rows = measure_windows(shape)
+        print(json.dumps({"metric": METRIC, "workload": "windows", "data": "synthetic", "n_gpus": 1,
+                          "decode_vs_allocated_window": rows}), flush=True)
         return
     if args.only == "ctxsweep":
         rows = measure_ctx_sweep(shape)

@@ -65,7 +65,7 @@ enum { HH_LOGITS_NONE = 0, HH_LOGITS_LAST = 1, HH_LOGITS_ALL = 2 };
 /*
  * Model and capacity description.  Supported: head_dim == 64, page_size == 16,
  * n_heads / n_kv_heads in {1, 2, 4, 8}, d_model % 64 == 0, ffn_dim % 8 == 0,
- * vocab >= 2, max_context <= 32768; anything else gives HH_ERR_UNSUPPORTED.  rms_eps is added to the mean square inside the root;
+ * vocab >= 2, max_context <= 131072; anything else gives HH_ERR_UNSUPPORTED.  rms_eps is added to the mean square inside the root;
  * rope_theta is the rotary base (frequencies theta^(-2i/head_dim)).
  */
 typedef struct {

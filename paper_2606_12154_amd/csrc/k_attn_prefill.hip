@@ -21,7 +21,7 @@
 
 namespace hh {
 
-constexpr int kFlashMaxPages = 2048;  // pages of keys per prefill attention (32768 positions)
+constexpr int kFlashMaxPages = 8192;  // pages of keys per prefill attention (131072 positions)
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 

@@ -452,7 +452,7 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ p
 // lane % 4) holds 16 dims of one key; scores use exp2 with 1/sqrt(64)*log2(e)
 // folded into q; each head keeps its own online softmax state.  The waves'
 // states are merged in LDS, one wave per head.
-constexpr int kRowsMaxPages = 2048;  // pages of one row (32768 positions)
+constexpr int kRowsMaxPages = 2048;  // pages of one row kept in LDS (32768 positions); later ones are read from the table
 
 template <typename TKV>
 struct KvPage {
@@ -484,7 +484,8 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
   const int s = row_stream[r], t = row_pos[r] + 1, npg = (t + kPage - 1) / kPage;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, key = lane >> 2, quarter = lane & 3;
   const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
-  for (int i = threadIdx.x; i < npg; i += 512) pts[i] = page_table[(size_t)s * L.max_pages + i];
+  for (int i = threadIdx.x; i < npg && i < kRowsMaxPages; i += 512) pts[i] = page_table[(size_t)s * L.max_pages + i];
+  auto page_of = [&](int pg) { return pg < kRowsMaxPages ? pts[pg] : page_table[(size_t)s * L.max_pages + pg]; };
   float qv[G][16];
 #pragma unroll
   for (int h = 0; h < G; ++h)
@@ -536,12 +537,12 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
   // Pages wave, wave + 8, ...; loads past the end re-read the row's last page.
   if (wave < npg) {
     KvPage<TKV> A, B;
-    kv_page_load(A, kv, L, layer, pts[wave], g, key, quarter);
+    kv_page_load(A, kv, L, layer, page_of(wave), g, key, quarter);
     for (int pg = wave; pg < npg; pg += 2 * NW) {
-      kv_page_load(B, kv, L, layer, pts[min(pg + NW, npg - 1)], g, key, quarter);
+      kv_page_load(B, kv, L, layer, page_of(min(pg + NW, npg - 1)), g, key, quarter);
       take(A, pg);
       if (pg + NW >= npg) break;
-      kv_page_load(A, kv, L, layer, pts[min(pg + 2 * NW, npg - 1)], g, key, quarter);
+      kv_page_load(A, kv, L, layer, page_of(min(pg + 2 * NW, npg - 1)), g, key, quarter);
       take(B, pg + NW);
     }
   }

@@ -62,7 +62,7 @@ bool config_supported(const hh_config& c, std::string& why) {
     why = "n_heads / n_kv_heads must be 1, 2, 4 or 8";
     return false;
   }
-  if (c.max_context > 32768) { why = "max_context must be at most 32768"; return false; }
+  if (c.max_context > 131072) { why = "max_context must be at most 131072"; return false; }
   if (c.d_model % 64 != 0) { why = "d_model must be a multiple of 64"; return false; }
   if (c.ffn_dim % 8 != 0) { why = "ffn_dim must be a multiple of 8"; return false; }
   if (c.d_model > 16384 || c.ffn_dim > 65536 || c.n_heads * 64 > 16384) { why = "dimension too large"; return false; }

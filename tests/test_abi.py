@@ -43,7 +43,7 @@ def test_workspace_sizes():
     ("ffn_dim", 690, hh.HH_ERR_UNSUPPORTED),
     ("dtype", 7, hh.HH_ERR_UNSUPPORTED),
     ("max_streams", 0, hh.HH_ERR_UNSUPPORTED),
-    ("max_context", 32769, hh.HH_ERR_UNSUPPORTED),
+    ("max_context", 131073, hh.HH_ERR_UNSUPPORTED),
     ("weight_format", 2, hh.HH_ERR_UNSUPPORTED),
     ("weight_format", hh.HH_WF_Q4G32, hh.HH_ERR_UNSUPPORTED),  # the tiny model is fp32
 ])

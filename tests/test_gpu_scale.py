@@ -75,7 +75,7 @@ def test_1b_32_streams_lockstep(one_b):
         ctx.close()
 
 
-@pytest.mark.parametrize("P", [8192, 32760])
+@pytest.mark.parametrize("P", [8192, 32760, 131064])
 def test_1b_long_context_kernel_paths_agree(one_b, P):
     shape, tensors = one_b
     toks = synth.make_tokens(shape.vocab, P + 3, 4)
