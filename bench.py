@@ -293,6 +293,57 @@ def measure_windows(shape):
     return rows
 
 
+def measure_e2e(shape):
+    """The serving path around the decoder (route, render, stream) on a
+    synthetic store shaped like the paper's routing study (563 entries from
+    17 documents, 1,126 queries drawn from entry vocabulary): routing
+    accuracy, gate rate and route latency over all queries (native BM25 on
+    the host), then 16 routed queries served end to end by the 1B bf16
+    decoder, 64 streamed tokens each: TTFT (query to first token on the
+    host), decode rate and end-to-end throughput, medians."""
+    import synth
+    from paper_2606_12154_amd import hh, serve
+    store = synth.make_store()
+    queries = synth.make_queries(store)
+    router = serve.Router([t for t, _ in store])
+    hit1 = hit3 = esc = ok = 0
+    lat = []
+    for q, want in queries:
+        ids, _ = router.top(q, 3)
+        hit1 += int(ids[0] == want)
+        hit3 += int(want in ids)
+        t0 = time.perf_counter()
+        e, m, x = router.route(q)
+        lat.append(time.perf_counter() - t0)
+        esc += int(x)
+        ok += int((not x) and e == want)
+    nq = len(queries)
+    routing = {"entries": len(store), "queries": nq, "top1": round(hit1 / nq, 4), "top3": round(hit3 / nq, 4),
+               "escalated": round(esc / nq, 4), "top1_of_answered": round(ok / max(1, nq - esc), 4),
+               "route_us_p50": round(float(np.median(lat)) * 1e6, 2)}
+    wl = synth.WORKLOADS["1b_decode"]
+    tensors = synth.make_weights(shape, wl["wseed"])
+    ctx = hh.Context(hh.make_config(shape, 1, 1024, 512))
+    ctx.load_weights(tensors)
+    del tensors
+    srv = serve.Server(ctx, router, [a for _, a in store], max_tokens=64)
+    answered = [q for q, _ in queries if not router.route(q)[2]][:17]
+    runs = []
+    for i, q in enumerate(answered):
+        a = srv.answer(q, 64)
+        if i > 0:  # the first request warms up
+            runs.append(a)
+    ctx.close()
+    router.close()
+    med = lambda f: round(float(np.median([f(a) for a in runs])), 3)
+    serving = {"requests": len(runs), "tokens_each": 64,
+               "prompt_tokens_p50": med(lambda a: a.prompt_tokens),
+               "route_render_ms_p50": med(lambda a: a.t_render * 1e3),
+               "ttft_ms_p50": med(lambda a: a.ttft_ms), "decode_tok_s_p50": med(lambda a: a.decode_tok_s),
+               "e2e_ms_p50": med(lambda a: a.t_last * 1e3), "e2e_tok_s_p50": med(lambda a: a.e2e_tok_s)}
+    return {"routing": routing, "serving": serving}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -301,7 +352,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--other-configs", action="store_true",
                     help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
-    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep", "windows", "q4decode"],
+    ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep", "windows", "q4decode",
+                                       "e2e"],
                     help="measure just this one of the other workloads (for a kernel trace of it); "
                          "prints its figures instead of the decode line")
     ap.add_argument("--cpu-decode-steps", type=int, default=8)
@@ -323,6 +375,10 @@ def main():
     if args.only == "q4decode":
         print(json.dumps({"metric": METRIC, "workload": "q4decode", "data": "synthetic", "n_gpus": 1,
                           **measure_q4_decode(shape)}), flush=True)
+        return
+    if args.only == "e2e":
+        print(json.dumps({"metric": METRIC, "workload": "e2e", "data": "synthetic", "n_gpus": 1,
+                          **measure_e2e(shape)}), flush=True)
         return
     if args.only == "windows":
         rows = measure_windows(shape)

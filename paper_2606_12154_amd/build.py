@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libhh.so")
 BUILD = os.path.join(ROOT, "_build")
-SOURCES = ["k_decode.hip", "k_gemm.hip", "k_attn_prefill.hip", "k_load.hip", "k_step.hip", "runtime.hip"]
+SOURCES = ["k_decode.hip", "k_gemm.hip", "k_attn_prefill.hip", "k_load.hip", "k_step.hip", "runtime.hip",
+           "router.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -39,7 +40,7 @@ def build(verbose: bool = False) -> str:
     jobs = []
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         for src in SOURCES:
-            obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+            obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
             objs.append(obj)
             cmd = [HIPCC] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
             jobs.append((src, ex.submit(_run, cmd)))

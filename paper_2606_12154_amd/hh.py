@@ -25,7 +25,8 @@ HH_WF_DTYPE, HH_WF_Q4G32 = 0, 1
 
 EXPORTED = ["hh_workspace_size", "hh_create", "hh_load_weights", "hh_prefill", "hh_decode_step",
             "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error",
-            "hh_q4g32_quantize"]
+            "hh_q4g32_quantize", "hh_router_create", "hh_router_query", "hh_router_route",
+            "hh_router_size", "hh_router_destroy", "hh_render_marker"]
 
 
 class hh_config(ctypes.Structure):
@@ -67,6 +68,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hh_destroy": ([c_void_p], None),
         "hh_last_error": ([c_void_p], ctypes.c_char_p),
         "hh_q4g32_quantize": ([c_void_p, ctypes.c_int64, c_int32, c_void_p, c_void_p], c_int32),
+        "hh_router_create": ([POINTER(ctypes.c_char_p), c_int32, c_float, c_float, POINTER(c_void_p)], c_int32),
+        "hh_router_query": ([c_void_p, ctypes.c_char_p, c_int32, i32p, POINTER(ctypes.c_double), i32p], c_int32),
+        "hh_router_route": ([c_void_p, ctypes.c_char_p, c_float, i32p, POINTER(ctypes.c_double), i32p], c_int32),
+        "hh_router_size": ([c_void_p, i32p, i32p], c_int32),
+        "hh_router_destroy": ([c_void_p], None),
+        "hh_render_marker": ([ctypes.c_char_p, c_void_p, ctypes.c_int64, POINTER(ctypes.c_int64)], c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -137,6 +144,55 @@ def hh_last_error(ctx: int) -> str:
 def hh_q4g32_quantize(src_ptr: int, rows: int, K: int, dst_ptr: int, hip_stream: int) -> None:
     _check(None, load_library().hh_q4g32_quantize(c_void_p(src_ptr), rows, K, c_void_p(dst_ptr),
                                                   c_void_p(hip_stream)))
+
+
+def _text(s) -> bytes:
+    return s.encode() if isinstance(s, str) else bytes(s)
+
+
+def hh_router_create(entries, k1: float = 1.2, b: float = 0.75) -> int:
+    raw = [_text(e) for e in entries]
+    arr = (ctypes.c_char_p * len(raw))(*raw)
+    r = c_void_p()
+    _check(None, load_library().hh_router_create(arr, len(raw), k1, b, byref(r)))
+    return r.value
+
+
+def hh_router_query(router: int, query, k: int):
+    """Returns (ids int32 array, scores float64 array), best first."""
+    ids = np.zeros(max(k, 1), dtype=np.int32)
+    sc = np.zeros(max(k, 1), dtype=np.float64)
+    n = c_int32()
+    _check(None, load_library().hh_router_query(router, _text(query), k, ids.ctypes.data_as(POINTER(c_int32)),
+                                                sc.ctypes.data_as(POINTER(ctypes.c_double)), byref(n)))
+    return ids[:n.value], sc[:n.value]
+
+
+def hh_router_route(router: int, query, tau: float = 0.05):
+    """Returns (entry, margin, escalate)."""
+    e, m, x = c_int32(), ctypes.c_double(), c_int32()
+    _check(None, load_library().hh_router_route(router, _text(query), tau, byref(e), byref(m), byref(x)))
+    return e.value, m.value, bool(x.value)
+
+
+def hh_router_size(router: int):
+    n, t = c_int32(), c_int32()
+    _check(None, load_library().hh_router_size(router, byref(n), byref(t)))
+    return n.value, t.value
+
+
+def hh_router_destroy(router: int) -> None:
+    load_library().hh_router_destroy(router)
+
+
+def hh_render_marker(answer) -> bytes:
+    need = ctypes.c_int64()
+    lib = load_library()
+    a = _text(answer)
+    lib.hh_render_marker(a, None, 0, byref(need))
+    buf = ctypes.create_string_buffer(max(need.value, 1))
+    _check(None, lib.hh_render_marker(a, buf, need.value, byref(need)))
+    return buf.raw[:need.value]
 
 
 def _check(ctx, status: int) -> None:

@@ -147,3 +147,56 @@ def make_tokens(vocab: int, n: int, seed: int) -> np.ndarray:
     """n uniform random token ids in [0, vocab) from PCG64(seed), int32."""
     rng = np.random.Generator(np.random.PCG64(seed))
     return rng.integers(0, vocab, size=n, dtype=np.int32)
+
+
+# ---------------------------------------------------------------- synthetic knowledge store
+
+_SYLLABLES = ["ka", "lo", "mi", "ne", "su", "ta", "ri", "po", "ve", "du", "an", "el", "or", "is", "um",
+              "bra", "cle", "dro", "fin", "gal", "hem", "jor", "kel", "mon", "nar", "pel", "quo", "ser",
+              "tin", "vor", "wex", "yal", "zer"]
+
+
+def _word(rng: np.random.Generator) -> str:
+    return "".join(rng.choice(_SYLLABLES, size=int(rng.integers(2, 5))))
+
+
+def make_store(n_entries: int = 563, n_documents: int = 17, seed: int = 0):
+    """A seeded synthetic store in the shape of the paper's routing study
+    (563 entries harvested from 17 documents): entries of one document share
+    its topic words, each entry has its own distinctive words, and every text
+    mixes in common words drawn Zipf-like from a shared vocabulary.  Returns
+    a list of (indexed text, answer line) pairs.  Plain text generation: no
+    scoring arithmetic."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 9001]))
+    common = sorted({_word(rng) for _ in range(400)})
+    zipf = 1.0 / np.arange(1, len(common) + 1)
+    zipf /= zipf.sum()
+    topics = [[_word(rng) for _ in range(30)] for _ in range(n_documents)]
+    doc_of = np.sort(rng.integers(0, n_documents, size=n_entries))
+    store = []
+    for i in range(n_entries):
+        own = [_word(rng) for _ in range(int(rng.integers(4, 9)))]
+        topic = list(rng.choice(topics[doc_of[i]], size=8, replace=False))
+        filler = list(rng.choice(common, size=int(rng.integers(20, 50)), p=zipf))
+        words = own + topic + filler
+        rng.shuffle(words)
+        text = " ".join(words)
+        answer = f"{own[0].capitalize()} {topic[0]} is {int(rng.integers(1, 10000))} {own[1]} as of {1990 + i % 35}."
+        store.append((text, answer))
+    return store
+
+
+def make_queries(store, per_entry: int = 2, seed: int = 1):
+    """Queries generated from each entry's own vocabulary (as the paper's
+    1,126 queries for 563 entries were): 3 to 6 of the entry's words, one
+    or two of them possibly shared with other entries.  Returns a list of
+    (query text, entry id)."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 9002]))
+    out = []
+    for i, (text, _) in enumerate(store):
+        words = text.split()
+        for _ in range(per_entry):
+            k = int(rng.integers(3, 7))
+            q = list(rng.choice(words, size=k, replace=False))
+            out.append((" ".join(q), i))
+    return out

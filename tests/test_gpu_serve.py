@@ -1,0 +1,68 @@
+"""The serving path on the GPU (tiny fp32 decoder): route, render, stream.
+The streamed ids are the device's greedy sequence (its argmax history), the
+oracle's greedy continuation of the rendered prompt up to the first near-tie,
+and an escalated query decodes nothing."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import new_context, top2_margin
+from oracle import router as orc
+from paper_2606_12154_amd import hh, serve
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tiny_server():
+    shape = synth.TINY
+    tensors = synth.make_weights(shape, 0, gain_std=0.1)
+    model = oracle.Decoder(shape, synth.weights_as_f64(shape, tensors))
+    store = synth.make_store(60, 4, seed=21)
+    ctx = new_context(shape, tensors, streams=2, context=256)
+    router = serve.Router([t for t, _ in store])
+    srv = serve.Server(ctx, router, [a for _, a in store], max_tokens=32, stream_id=1)
+    yield shape, model, store, ctx, srv
+    router.close()
+    ctx.close()
+
+
+def test_streamed_tokens_are_the_greedy_sequence(tiny_server):
+    shape, model, store, ctx, srv = tiny_server
+    queries = synth.make_queries(store, 1, seed=22)
+    served = 0
+    for q, want in queries[:12]:
+        e, m, esc = orc.route([t for t, _ in store], q)
+        a = srv.answer(q, 24)
+        assert (a.entry, a.escalated) == (e, esc)
+        if esc:
+            assert a.tokens == []
+            continue
+        served += 1
+        prompt = serve.byte_tokens(orc.render_marker(store[e][1]).encode())
+        assert a.prompt_tokens == len(prompt)
+        assert len(a.tokens) == 24
+        hist = ctx.read_argmax(1, len(prompt) - 1, 24)
+        assert list(hist) == a.tokens
+        assert 0 < a.t_route <= a.t_render <= a.t_first <= a.t_last
+        # Oracle greedy continuation, compared up to its first near-tie.
+        logits, cache = model.prefill(prompt, rows="last")
+        row = logits[0]
+        for i, tok in enumerate(a.tokens):
+            if top2_margin(row) <= 1e-2:
+                break
+            assert tok == int(np.argmax(row)), f"token {i} of query {q!r}"
+            row = model.decode(cache, tok)
+    assert served >= 8
+    print(f"served {served} of 12 queries")
+
+
+def test_escalated_query_decodes_nothing(tiny_server):
+    shape, model, store, ctx, srv = tiny_server
+    before = ctx.length(1)
+    a = srv.answer("zzzz qqqq", 8)
+    assert a.escalated and a.margin == 0.0 and a.tokens == []
+    assert ctx.length(1) == before
+    with pytest.raises(ValueError):
+        srv.answer(synth.make_queries(store, 1, seed=22)[0][0], 33)
