@@ -439,6 +439,21 @@ def main():
     gen = ctx.read_argmax(0, P - 1, N + 1)
     assert gen.min() >= 0 and gen.max() < shape.vocab
 
+    # Achievable read bandwidth on this device: a plain streaming read of
+    # 4 GiB (the library's read probe), 10 timed passes after 2 warm ones.
+    probe = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
+    p0 = torch.cuda.Event(enable_timing=True)
+    p1 = torch.cuda.Event(enable_timing=True)
+    for _ in range(2):
+        hh.hh_read_probe(probe.data_ptr(), probe.numel(), st.cuda_stream)
+    p0.record(st)
+    for _ in range(10):
+        hh.hh_read_probe(probe.data_ptr(), probe.numel(), st.cuda_stream)
+    p1.record(st)
+    p1.synchronize()
+    read_gbs = 10 * probe.numel() / (p0.elapsed_time(p1) / 1e3) / 1e9
+    del probe
+
     dec_s = float(np.sum(decs))
     tok_s = args.steps * N / dec_s
     launch_s = dec_s / (args.steps * N)          # one persistent-kernel launch per token
@@ -467,11 +482,15 @@ def main():
         "ttft_ms_min": round(float(np.min(ttfts)) * 1e3, 3),
         "ttft_ms_max": round(float(np.max(ttfts)) * 1e3, 3),
         "decode_ms_per_token": round(launch_s * 1e3, 4),
+        "decode_tok_s_min": round(N / max(decs), 2),
+        "decode_tok_s_max": round(N / min(decs), 2),
         "e2e_tok_s": round(args.steps * (N + 1) / wall, 2),
         "roofline": {"bound": "hbm", "kernel": "k_decode_step (one launch per token)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "bytes_per_launch": int(launch_bytes), "launch_us": round(launch_s * 1e6, 2)},
+                     "bytes_per_launch": int(launch_bytes), "launch_us": round(launch_s * 1e6, 2),
+                     "measured_read_gbs": round(read_gbs, 1),
+                     "frac_of_measured_read": round(achieved / read_gbs, 4)},
     }
 
     if args.other_configs:

@@ -181,6 +181,15 @@ hh_status hh_q4g32_quantize(const uint16_t* src, int64_t rows, int32_t K, uint8_
 /* Destroy the host context (the arena stays the caller's). NULL is a no-op. */
 void hh_destroy(hh_ctx* ctx);
 
+/* Measurement aid, not a step of the decoder: enqueue on hip_stream one pass
+ * that reads `bytes` of device memory at src once (16-byte vector loads from
+ * every CU) and computes nothing visible.  Timed by the caller with events,
+ * it gives the read bandwidth a kernel can reach on the device, the
+ * reference the decode kernel's HBM fraction is also reported against.
+ * src must be device memory, 16-byte aligned, bytes a positive multiple of
+ * 16; otherwise HH_ERR_INVALID_ARG. */
+hh_status hh_read_probe(const void* src, size_t bytes, void* hip_stream);
+
 /* Message of the last error on this context ("" if none); never NULL. */
 const char* hh_last_error(const hh_ctx* ctx);
 

@@ -915,3 +915,18 @@ hh_status hh_q4g32_quantize(const uint16_t* src, int64_t rows, int32_t K, uint8_
 }
 
 }  // extern "C"
+
+namespace hh {
+void read_probe(hipStream_t st, const void* src, size_t bytes);  // k_load.hip
+}
+
+extern "C" {
+
+hh_status hh_read_probe(const void* src, size_t bytes, void* hip_stream) {
+  if (!src || bytes < 16 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(src) % 16 != 0) return HH_ERR_INVALID_ARG;
+  if (!is_device_ptr(src)) return HH_ERR_INVALID_ARG;
+  read_probe(static_cast<hipStream_t>(hip_stream), src, bytes);
+  return hipGetLastError() == hipSuccess ? HH_OK : HH_ERR_HIP;
+}
+
+}  // extern "C"

@@ -26,7 +26,7 @@ HH_WF_DTYPE, HH_WF_Q4G32 = 0, 1
 EXPORTED = ["hh_workspace_size", "hh_create", "hh_load_weights", "hh_prefill", "hh_decode_step",
             "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error",
             "hh_q4g32_quantize", "hh_router_create", "hh_router_query", "hh_router_route",
-            "hh_router_size", "hh_router_destroy", "hh_render_marker"]
+            "hh_router_size", "hh_router_destroy", "hh_render_marker", "hh_read_probe"]
 
 
 class hh_config(ctypes.Structure):
@@ -74,6 +74,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hh_router_size": ([c_void_p, i32p, i32p], c_int32),
         "hh_router_destroy": ([c_void_p], None),
         "hh_render_marker": ([ctypes.c_char_p, c_void_p, ctypes.c_int64, POINTER(ctypes.c_int64)], c_int32),
+        "hh_read_probe": ([c_void_p, c_size_t, c_void_p], c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -144,6 +145,10 @@ def hh_last_error(ctx: int) -> str:
 def hh_q4g32_quantize(src_ptr: int, rows: int, K: int, dst_ptr: int, hip_stream: int) -> None:
     _check(None, load_library().hh_q4g32_quantize(c_void_p(src_ptr), rows, K, c_void_p(dst_ptr),
                                                   c_void_p(hip_stream)))
+
+
+def hh_read_probe(src_ptr: int, nbytes: int, hip_stream: int) -> None:
+    _check(None, load_library().hh_read_probe(c_void_p(src_ptr), nbytes, c_void_p(hip_stream)))
 
 
 def _text(s) -> bytes:

@@ -95,3 +95,12 @@ def test_q4_quantize_rejects_bad_arguments():
     with pytest.raises(hh.HHError) as e:
         hh.hh_q4g32_quantize(0, 4, 64, 1 << 21, 0)
     assert e.value.status == hh.HH_ERR_INVALID_ARG
+
+
+def test_read_probe_rejects_bad_arguments():
+    import numpy as np
+    host = np.zeros(64, dtype=np.uint8)
+    for ptr, n in [(host.ctypes.data, 64), (0, 64), (host.ctypes.data, 15)]:
+        with pytest.raises(hh.HHError) as e:
+            hh.hh_read_probe(ptr, n, 0)
+        assert e.value.status == hh.HH_ERR_INVALID_ARG
