@@ -356,7 +356,7 @@ def main():
                                        "e2e"],
                     help="measure just this one of the other workloads (for a kernel trace of it); "
                          "prints its figures instead of the decode line")
-    ap.add_argument("--cpu-decode-steps", type=int, default=8)
+    ap.add_argument("--cpu-decode-steps", type=int, default=256)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()

@@ -161,21 +161,23 @@ template void transpose<_Float16>(hipStream_t, const _Float16*, _Float16*, int, 
 
 // ---------------------------------------------------------------- read probe
 
-// Streams n 16-byte vectors once (non-temporal loads, four in flight per
-// thread) and folds them into a value that is stored only if it matches a
-// constant, so the loads cannot be dropped.
+// Streams n 16-byte vectors once (non-temporal loads, eight in flight per
+// thread, 32768 workgroups: the fastest of the shapes tried) and folds them
+// into a value that is stored only if it matches a constant, so the loads
+// cannot be dropped.
 __device__ unsigned g_probe_sink;
 
 __global__ __launch_bounds__(256) void k_read_probe(const u32x4* __restrict__ p, size_t n) {
+  constexpr int U = 8;
   const size_t stride = (size_t)gridDim.x * 256;
   size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   unsigned acc = 0;
-  for (; i + 3 * stride < n; i += 4 * stride) {
-    const u32x4 a = __builtin_nontemporal_load(p + i);
-    const u32x4 b = __builtin_nontemporal_load(p + i + stride);
-    const u32x4 c = __builtin_nontemporal_load(p + i + 2 * stride);
-    const u32x4 e = __builtin_nontemporal_load(p + i + 3 * stride);
-    acc ^= (a.x ^ b.y ^ c.z ^ e.w) + (a.y ^ b.z ^ c.w ^ e.x) + (a.z ^ b.w ^ c.x ^ e.y) + (a.w ^ b.x ^ c.y ^ e.z);
+  for (; i + (U - 1) * stride < n; i += U * stride) {
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc ^= v[u].x + v[u].y + v[u].z + v[u].w;
   }
   for (; i < n; i += stride) {
     const u32x4 a = __builtin_nontemporal_load(p + i);
@@ -186,7 +188,7 @@ __global__ __launch_bounds__(256) void k_read_probe(const u32x4* __restrict__ p,
 
 void read_probe(hipStream_t st, const void* src, size_t bytes) {
   const size_t n = bytes / 16;
-  k_read_probe<<<2048, 256, 0, st>>>(reinterpret_cast<const u32x4*>(src), n);
+  k_read_probe<<<32768, 256, 0, st>>>(reinterpret_cast<const u32x4*>(src), n);
 }
 
 }  // namespace hh
