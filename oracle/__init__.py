@@ -26,6 +26,10 @@ example, exact round trips of representable groups, the half-step error
 bound, ties to even, zero groups and the nibble layout.  Matching the paper's
 own model outputs is parity unpinned: its weights and printed outputs do not
 exist, and neither does its 4-bit format's definition.
+
+``router.py`` is the oracle of the serving steps around the decoder (BM25
+routing with the margin gate, the marker-line envelope), pinned in
+``tests/test_router.py``; it is imported as ``oracle.router``.
 """
 from .decoder import (Decoder, KVCache, apply_rope, attention, greedy, rms_norm,
                       rope_angles, silu)

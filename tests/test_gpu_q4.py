@@ -10,6 +10,8 @@
   one-row MFMA decode path (HH_STEP_KERNEL=0) and four lockstep streams are
   within max-abs 2e-2, argmax equal where the oracle's top-2 margin exceeds
   1e-2.
+* At 8,192 cached positions the persistent kernel on the 4-bit rows and the
+  graph path on the exact fp16 copies agree within the same bound.
 """
 import os
 
@@ -18,7 +20,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import check_logits, new_context
+from gpu_util import check_logits, new_context, top2_margin
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -118,3 +120,36 @@ def test_q4_one_row_mfma_path_and_streams(q4_model):
         print(f"1B 4-bit multi-stream and one-row paths: max-abs {worst:.4g}")
     finally:
         ctx.close()
+
+
+def test_q4_long_context_kernel_paths_agree(q4_model):
+    """8,192 cached positions: attention items take part of the workgroups,
+    so the 4-bit gate/up/down split differs per workgroup; the persistent
+    kernel on 4-bit rows must agree with the graph path on the fp16 copies."""
+    shape, tensors, _ = q4_model
+    P = 8192
+    toks = synth.make_tokens(shape.vocab, P + 3, 7)
+    step_ctx = q4_context(shape, tensors, streams=1, context=P + 8, max_prefill=2048)
+    os.environ["HH_STEP_KERNEL"] = "0"
+    try:
+        graph_ctx = q4_context(shape, tensors, streams=1, context=P + 8, max_prefill=2048)
+    finally:
+        del os.environ["HH_STEP_KERNEL"]
+    try:
+        step_ctx.prefill(0, toks[:P])
+        graph_ctx.prefill(0, toks[:P])
+        worst = 0.0
+        for t in toks[P:]:
+            _, a = step_ctx.decode_step([0], [int(t)], logits=True)
+            _, b = graph_ctx.decode_step([0], [int(t)], logits=True)
+            a, b = np.asarray(a[0], np.float64), np.asarray(b[0], np.float64)
+            assert np.isfinite(a).all() and np.isfinite(b).all()
+            d = float(np.abs(a - b).max())
+            worst = max(worst, d)
+            assert d <= TOL, f"paths differ by {d:.3g}"
+            if top2_margin(b) > 2e-2:
+                assert int(np.argmax(a)) == int(np.argmax(b))
+        print(f"1B 4-bit decode at {P} positions, kernel vs graph path: max-abs {worst:.3g}")
+    finally:
+        step_ctx.close()
+        graph_ctx.close()
