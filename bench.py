@@ -300,7 +300,8 @@ def measure_e2e(shape):
     accuracy, gate rate and route latency over all queries (native BM25 on
     the host), then 16 routed queries served end to end by the 1B bf16
     decoder, 64 streamed tokens each: TTFT (query to first token on the
-    host), decode rate and end-to-end throughput, medians."""
+    host), decode rate and end-to-end throughput, medians; then 32 routed
+    queries served at once (lockstep decode over 32 streams)."""
     import synth
     from paper_2606_12154_amd import hh, serve
     store = synth.make_store()
@@ -323,25 +324,37 @@ def measure_e2e(shape):
                "route_us_p50": round(float(np.median(lat)) * 1e6, 2)}
     wl = synth.WORKLOADS["1b_decode"]
     tensors = synth.make_weights(shape, wl["wseed"])
-    ctx = hh.Context(hh.make_config(shape, 1, 1024, 512))
+    ctx = hh.Context(hh.make_config(shape, 32, 1024, 512))
     ctx.load_weights(tensors)
     del tensors
-    srv = serve.Server(ctx, router, [a for _, a in store], max_tokens=64)
-    answered = [q for q, _ in queries if not router.route(q)[2]][:17]
+    srv = serve.Server(ctx, router, [a for _, a in store], max_tokens=64, max_batch=32)
+    answered = [q for q, _ in queries if not router.route(q)[2]]
     runs = []
-    for i, q in enumerate(answered):
+    for i, q in enumerate(answered[:17]):
         a = srv.answer(q, 64)
         if i > 0:  # the first request warms up
             runs.append(a)
+    # 32 requests at once: prefilled one by one into their own streams, then
+    # decoded in lockstep (the second batch is timed).
+    for rep in range(2):
+        batch = srv.answer_batch(answered[32 * rep:32 * rep + 32], 64, list(range(32)))
     ctx.close()
     router.close()
+    t_end = max(a.t_last for a in batch)
+    batched = {"requests": len(batch), "tokens_each": 64,
+               "ttft_ms_p50": round(float(np.median([a.ttft_ms for a in batch])), 3),
+               "ttft_ms_max": round(max(a.ttft_ms for a in batch), 3),
+               "e2e_ms": round(t_end * 1e3, 3),
+               "aggregate_tok_s": round(sum(len(a.tokens) for a in batch) / t_end, 1),
+               "lockstep_decode_tok_s": round(sum(len(a.tokens) - 1 for a in batch) /
+                                              (t_end - max(a.t_first for a in batch)), 1)}
     med = lambda f: round(float(np.median([f(a) for a in runs])), 3)
     serving = {"requests": len(runs), "tokens_each": 64,
                "prompt_tokens_p50": med(lambda a: a.prompt_tokens),
                "route_render_ms_p50": med(lambda a: a.t_render * 1e3),
                "ttft_ms_p50": med(lambda a: a.ttft_ms), "decode_tok_s_p50": med(lambda a: a.decode_tok_s),
                "e2e_ms_p50": med(lambda a: a.t_last * 1e3), "e2e_tok_s_p50": med(lambda a: a.e2e_tok_s)}
-    return {"routing": routing, "serving": serving}
+    return {"routing": routing, "serving": serving, "serving_32_at_once": batched}
 
 
 def main():

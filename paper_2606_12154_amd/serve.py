@@ -91,13 +91,15 @@ class Server:
     already queued."""
 
     def __init__(self, ctx: "hh.Context", router: Router, answers: Sequence[str], max_tokens: int,
-                 stream_id: int = 0, tau: float = TAU):
+                 stream_id: int = 0, tau: float = TAU, max_batch: int = 1):
         import torch
         self.torch = torch
         self.ctx, self.router, self.answers = ctx, router, list(answers)
         self.stream_id, self.tau, self.max_tokens = stream_id, tau, max_tokens
-        self.dev = torch.zeros(max_tokens, dtype=torch.int32, device=ctx.device)
-        self.host = torch.zeros(max_tokens, dtype=torch.int32, pin_memory=True)
+        self.max_batch = max_batch
+        # Token slots [step][request]; one event per step.
+        self.dev = torch.zeros((max_tokens, max_batch), dtype=torch.int32, device=ctx.device)
+        self.host = torch.zeros((max_tokens, max_batch), dtype=torch.int32, pin_memory=True)
         self.events = [torch.cuda.Event() for _ in range(max_tokens)]
         self.ids = np.array([stream_id], dtype=np.int32)
 
@@ -126,11 +128,11 @@ class Server:
         with torch.cuda.stream(st):
             for i in range(1, n_tokens):
                 hh.hh_decode_step(self.ctx.ctx, 1, self.ids, None, None, self.dev[i].data_ptr())
-                self.host[i].copy_(self.dev[i], non_blocking=True)
+                self.host[i, 0:1].copy_(self.dev[i, 0:1], non_blocking=True)
                 self.events[i].record(st)
         for i in range(1, n_tokens):
             self.events[i].synchronize()
-            tok = int(self.host[i])
+            tok = int(self.host[i, 0])
             a.tokens.append(tok)
             a.t_last = time.perf_counter() - t0
             yield tok
@@ -142,3 +144,54 @@ class Server:
         for _ in self.stream(query, n_tokens, a):
             pass
         return a
+
+    def answer_batch(self, queries: Sequence[str], n_tokens: int, streams: Sequence[int]) -> List[Answer]:
+        """Serve several queries at once: each routed query is rendered and
+        prefilled into its own decoder stream (``streams[i]`` for query i),
+        then all of them decode in lockstep (one multi-stream step per token,
+        device-fed), every step's tokens copied behind one event.  Escalated
+        queries take no stream time.  Clocks run from the batch's arrival."""
+        if not 1 <= n_tokens <= self.max_tokens:
+            raise ValueError(f"n_tokens must be in 1..{self.max_tokens}")
+        if len(queries) != len(streams) or len(queries) > self.max_batch:
+            raise ValueError(f"need one stream per query and at most {self.max_batch} queries")
+        torch = self.torch
+        t0 = time.perf_counter()
+        out: List[Answer] = []
+        live: List[int] = []
+        for i, q in enumerate(queries):
+            entry, margin, esc = self.router.route(q, self.tau)
+            a = Answer(entry, margin, esc)
+            a.t_route = time.perf_counter() - t0
+            out.append(a)
+            if not esc:
+                live.append(i)
+        for i in live:
+            a = out[i]
+            ids = byte_tokens(hh.hh_render_marker(self.answers[a.entry]))
+            a.prompt_tokens = len(ids)
+            a.t_render = time.perf_counter() - t0
+            self.ctx.reset(streams[i])
+            first, _ = self.ctx.prefill(streams[i], ids)
+            a.t_first = time.perf_counter() - t0
+            a.tokens.append(first)
+        n = len(live)
+        if n == 0 or n_tokens == 1:
+            for i in live:
+                out[i].t_last = out[i].t_first
+            return out
+        sids = np.array([streams[i] for i in live], dtype=np.int32)
+        st = self.ctx.stream
+        with torch.cuda.stream(st):
+            for k in range(1, n_tokens):
+                hh.hh_decode_step(self.ctx.ctx, n, sids, None, None, self.dev[k].data_ptr())
+                self.host[k, :n].copy_(self.dev[k, :n], non_blocking=True)
+                self.events[k].record(st)
+        for k in range(1, n_tokens):
+            self.events[k].synchronize()
+            now = time.perf_counter() - t0
+            row = self.host[k, :n].tolist()
+            for j, i in enumerate(live):
+                out[i].tokens.append(int(row[j]))
+                out[i].t_last = now
+        return out
