@@ -521,6 +521,8 @@ hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, f
   if (rc != HH_OK) return rc;
   const int chunk = L.rows_cap;
   float* lbuf = c->at<float>(L.logits);
+  // The prefill rows overwrite row_stream: the next decode uploads its ids.
+  c->uploaded_streams.clear();
   for (int r0 = 0; r0 < n; r0 += chunk) {
     const int P = std::min(chunk, n - r0);
     const bool last = r0 + P == n;

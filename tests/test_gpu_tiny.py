@@ -101,6 +101,30 @@ def test_multistream_lockstep(tiny):
         assert ctx.length(s) == n + 6
 
 
+def test_prefill_between_lockstep_steps(tiny):
+    """A prefill into another stream between two decode steps over the same
+    stream list: the prefill's rows reuse the row-stream table, so the second
+    step must not take the table for still uploaded (regression)."""
+    shape, tensors, model = tiny
+    ctx = new_context(shape, tensors, streams=6)
+    ids = [0, 1, 2]
+    caches = []
+    for s in ids:
+        p = synth.make_tokens(shape.vocab, 9 + 5 * s, 200 + s)
+        ctx.prefill(s, p)
+        caches.append(model.prefill(p, rows="last")[1])
+    rng = np.random.default_rng(8)
+    for step in range(3):
+        if step == 1:
+            ctx.prefill(5, synth.make_tokens(shape.vocab, 12, 299))  # rows 0..11 name stream 5
+        feed = rng.integers(0, shape.vocab, size=3).astype(np.int32)
+        _, lg = ctx.decode_step(ids, feed, logits=True)
+        for k, s in enumerate(ids):
+            check_logits(lg[k], model.decode(caches[s], int(feed[k])), TOL, what=f"step {step} stream {s}")
+    assert [ctx.length(s) for s in ids] == [9 + 5 * s + 3 for s in ids]
+    assert ctx.length(5) == 12
+
+
 def test_chunked_and_appended_prefill(tiny):
     shape, tensors, model = tiny
     toks = synth.make_tokens(shape.vocab, 70, 3)
