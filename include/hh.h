@@ -133,6 +133,26 @@ hh_status hh_prefill(hh_ctx* ctx, int32_t stream_id, const int32_t* tokens, int3
                      int32_t logits_mode, float* logits, int32_t* next_token);
 
 /*
+ * Prompt evaluation for several streams in one pass (several requests
+ * arriving together, the paper's runtime phase at more than one user): the
+ * prompts of n distinct streams are appended as one set of rows, every layer
+ * runs once over all of them (each row attends to its own stream's keys up
+ * to its position), and the greedy next token of each stream comes from its
+ * last row, as hh_prefill would give it.
+ *  stream_ids   host, n distinct ids; lengths host, n counts >= 1.
+ *  tokens       host, the prompts concatenated in stream_ids order
+ *               (sum of lengths ids in [0, vocab)); the sum must not exceed
+ *               the rows of one pass (max_prefill, or max_context when 0,
+ *               and at least max_streams).
+ *  next_tokens  NULL or n int32 (host or device), in stream_ids order.
+ * The call waits for its pass to finish.  Errors: INVALID_ARG (n outside
+ * 1..max_streams, an id out of range or repeated, a length < 1, too many
+ * rows, a token out of range), CONTEXT_FULL, NOT_LOADED, HIP.
+ */
+hh_status hh_prefill_batch(hh_ctx* ctx, int32_t n, const int32_t* stream_ids, const int32_t* lengths,
+                           const int32_t* tokens, int32_t* next_tokens);
+
+/*
  * One greedy decode step of n_streams streams in lockstep: each listed stream
  * consumes one token at its current length and advances by one.
  *  stream_ids   host, n_streams distinct ids; NULL means 0..n_streams-1.

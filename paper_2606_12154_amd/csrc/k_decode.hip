@@ -24,11 +24,13 @@ __global__ __launch_bounds__(256) void k_prep_embed(int prefill_stream, const in
                                                     int* __restrict__ row_stream, int* __restrict__ row_pos,
                                                     const int* __restrict__ pos, const int* __restrict__ pending,
                                                     const TW* __restrict__ embed, float* __restrict__ x, int d) {
+  // prefill_stream >= 0: rows r of that stream at positions pos + r; -1: one
+  // row per listed stream at its position; -2: row_stream and row_pos given.
   const int r = blockIdx.x;
   const int s = prefill_stream >= 0 ? prefill_stream : row_stream[r];
-  const int p = pos[s] + (prefill_stream >= 0 ? r : 0);
+  const int p = prefill_stream == -2 ? row_pos[r] : pos[s] + (prefill_stream >= 0 ? r : 0);
   const int tok = feed ? feed[r] : pending[s];
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == 0 && prefill_stream != -2) {
     row_pos[r] = p;
     if (prefill_stream >= 0) row_stream[r] = s;
   }

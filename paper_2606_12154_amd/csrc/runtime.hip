@@ -553,6 +553,71 @@ hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, f
   return HH_OK;
 }
 
+// Prompts of several streams in one pass: the rows of all of them through
+// every layer (attention per row over its own stream's keys), then the head
+// on the last row of each.
+template <typename TW, typename TKV, typename TM>
+hh_status do_prefill_batch(hh_ctx* c, int n, const int32_t* ids, const int32_t* lens, const int32_t* tokens,
+                           int32_t* next) {
+  const Layout& L = c->L;
+  using DK = DecodeKernels<TW, TKV, TM>;
+  using GK = GemmKernels<TM, TKV>;
+  hipStream_t st = c->stream;
+  const hh_config& g = c->cfg;
+  const int d = g.d_model;
+  for (int i = 0; i < n; ++i) {
+    hh_status rc = ensure_pages(c, ids[i], c->len[ids[i]] + lens[i]);
+    if (rc != HH_OK) return rc;
+  }
+  std::vector<int> rs, rp, last_s(n), last_p(n), last_r(n);
+  for (int i = 0; i < n; ++i) {
+    for (int j = 0; j < lens[i]; ++j) {
+      rs.push_back(ids[i]);
+      rp.push_back(c->len[ids[i]] + j);
+    }
+    last_r[i] = (int)rs.size() - 1;
+    last_s[i] = ids[i];
+    last_p[i] = rp.back();
+  }
+  const int R = (int)rs.size();
+  c->uploaded_streams.clear();
+  int* row_stream = c->at<int>(L.row_stream);
+  int* row_pos = c->at<int>(L.row_pos);
+  HIPCHK(c, hipMemcpyAsync(row_stream, rs.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
+  HIPCHK(c, hipMemcpyAsync(row_pos, rp.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
+  HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, R * sizeof(int), hipMemcpyHostToDevice, st));
+  float* x = c->at<float>(L.x);
+  DK::prep_embed(st, R, -2, c->at<int>(L.feed), row_stream, row_pos, c->at<int>(L.pos), c->at<int>(L.pending),
+                 c->at<TW>(L.embed), x, d);
+  enqueue_layers<TW, TKV, TM>(c, R, false, 1, -2, nullptr);
+  // Last rows to rows 0 .. n-1 (row i's source lies at or after row i and
+  // after every earlier destination), then the n-row head and argmax.
+  for (int i = 0; i < n; ++i)
+    if (last_r[i] != i)
+      HIPCHK(c, hipMemcpyAsync(x + (size_t)i * d, x + (size_t)last_r[i] * d, d * sizeof(float),
+                               hipMemcpyDeviceToDevice, st));
+  HIPCHK(c, hipMemcpyAsync(row_stream, last_s.data(), n * sizeof(int), hipMemcpyHostToDevice, st));
+  HIPCHK(c, hipMemcpyAsync(row_pos, last_p.data(), n * sizeof(int), hipMemcpyHostToDevice, st));
+  const float* fn = c->at<float>(L.final_norm);
+  unsigned long long* slot = c->at<unsigned long long>(L.slot);
+  TM* h = c->at<TM>(L.h);
+  const GemmWorkspace gws{c->at<float>(L.gemm_ws), L.gemm_ws_bytes};
+  if (GK::norm_fusable(d)) GK::rmsnorm(st, n, x, d, fn, g.rms_eps, h);
+  else DK::rmsnorm_rows(st, n, x, fn, g.rms_eps, d, h);
+  GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, g.vocab, 1.f / c->wscale, nullptr, slot, row_stream,
+             L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16));
+  finalize(st, 0, n, row_stream, row_pos, slot, c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos),
+           g.max_context);
+  HIPCHK(c, hipGetLastError());
+  if (next)
+    for (int i = 0; i < n; ++i)
+      HIPCHK(c, hipMemcpyAsync(next + i, c->at<int>(L.pending) + ids[i], sizeof(int), hipMemcpyDefault, st));
+  // The host arrays above are read by the copies: wait for them.
+  HIPCHK(c, hipStreamSynchronize(st));
+  for (int i = 0; i < n; ++i) c->len[ids[i]] += lens[i];
+  return HH_OK;
+}
+
 template <typename TW, typename TKV, typename TM>
 hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t* tokens, float* logits,
                     int32_t* next) {
@@ -827,6 +892,35 @@ hh_status hh_prefill(hh_ctx* c, int32_t s, const int32_t* tokens, int32_t n, int
                                     : do_prefill<float, float, float>(c, s, tokens, n, mode, logits, next);
   if (rc != HH_OK) return rc;
   return finish(c, (logits && !is_device_ptr(logits)) || (next && !is_device_ptr(next)));
+}
+
+hh_status hh_prefill_batch(hh_ctx* c, int32_t n, const int32_t* stream_ids, const int32_t* lengths,
+                           const int32_t* tokens, int32_t* next_tokens) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  if (!c->loaded) return c->fail(HH_ERR_NOT_LOADED, "weights not loaded");
+  const hh_config& g = c->cfg;
+  if (n < 1 || n > g.max_streams || !stream_ids || !lengths || !tokens)
+    return c->fail(HH_ERR_INVALID_ARG, "need 1..max_streams streams, their lengths and tokens");
+  std::vector<char> seen(g.max_streams, 0);
+  long long total = 0;
+  for (int i = 0; i < n; ++i) {
+    const int s = stream_ids[i];
+    if (s < 0 || s >= g.max_streams) return c->fail(HH_ERR_INVALID_ARG, "stream id out of range");
+    if (seen[s]) return c->fail(HH_ERR_INVALID_ARG, "stream listed twice");
+    seen[s] = 1;
+    if (lengths[i] < 1) return c->fail(HH_ERR_INVALID_ARG, "every prompt needs at least one token");
+    if ((long long)c->len[s] + lengths[i] > g.max_context)
+      return c->fail(HH_ERR_CONTEXT_FULL, "prompt exceeds max_context");
+    total += lengths[i];
+  }
+  if (total > c->L.rows_cap) return c->fail(HH_ERR_INVALID_ARG, "prompts exceed the rows of one prefill pass");
+  for (long long i = 0; i < total; ++i)
+    if (tokens[i] < 0 || tokens[i] >= g.vocab) return c->fail(HH_ERR_INVALID_ARG, "token id out of range");
+  hh_status rc = g.dtype == HH_BF16
+                     ? do_prefill_batch<__bf16, _Float16, _Float16>(c, n, stream_ids, lengths, tokens, next_tokens)
+                     : do_prefill_batch<float, float, float>(c, n, stream_ids, lengths, tokens, next_tokens);
+  if (rc != HH_OK) return rc;
+  return finish(c, next_tokens && !is_device_ptr(next_tokens));
 }
 
 hh_status hh_decode_step(hh_ctx* c, int32_t n, const int32_t* stream_ids, const int32_t* tokens, float* logits,

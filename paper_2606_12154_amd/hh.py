@@ -23,7 +23,7 @@ HH_F32, HH_BF16 = 0, 1
 HH_LOGITS_NONE, HH_LOGITS_LAST, HH_LOGITS_ALL = 0, 1, 2
 HH_WF_DTYPE, HH_WF_Q4G32 = 0, 1
 
-EXPORTED = ["hh_workspace_size", "hh_create", "hh_load_weights", "hh_prefill", "hh_decode_step",
+EXPORTED = ["hh_workspace_size", "hh_create", "hh_load_weights", "hh_prefill", "hh_prefill_batch", "hh_decode_step",
             "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error",
             "hh_q4g32_quantize", "hh_router_create", "hh_router_query", "hh_router_route",
             "hh_router_size", "hh_router_destroy", "hh_render_marker", "hh_read_probe"]
@@ -62,6 +62,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hh_load_weights": ([c_void_p, POINTER(c_void_p), c_int32], c_int32),
         "hh_prefill": ([c_void_p, c_int32, i32p, c_int32, c_int32, c_void_p, c_void_p], c_int32),
         "hh_decode_step": ([c_void_p, c_int32, i32p, i32p, c_void_p, c_void_p], c_int32),
+        "hh_prefill_batch": ([c_void_p, c_int32, i32p, i32p, i32p, c_void_p], c_int32),
         "hh_reset": ([c_void_p, c_int32], c_int32),
         "hh_stream_length": ([c_void_p, c_int32, i32p], c_int32),
         "hh_read_argmax": ([c_void_p, c_int32, c_int32, c_int32, i32p], c_int32),
@@ -108,6 +109,16 @@ def hh_prefill(ctx: int, stream_id: int, tokens: np.ndarray, logits_mode: int, l
     tokens = np.ascontiguousarray(tokens, dtype=np.int32)
     _check(ctx, load_library().hh_prefill(ctx, stream_id, tokens.ctypes.data_as(POINTER(c_int32)), len(tokens),
                                           logits_mode, logits_ptr, next_ptr))
+
+
+def hh_prefill_batch(ctx: int, stream_ids, prompts, next_ptr) -> None:
+    ids = np.ascontiguousarray(stream_ids, dtype=np.int32)
+    lens = np.array([len(p) for p in prompts], dtype=np.int32)
+    toks = np.ascontiguousarray(np.concatenate([np.asarray(p, dtype=np.int32) for p in prompts])
+                                if len(prompts) else np.zeros(0, np.int32), dtype=np.int32)
+    _check(ctx, load_library().hh_prefill_batch(ctx, len(ids), ids.ctypes.data_as(POINTER(c_int32)),
+                                                lens.ctypes.data_as(POINTER(c_int32)),
+                                                toks.ctypes.data_as(POINTER(c_int32)), next_ptr))
 
 
 def hh_decode_step(ctx: int, n_streams: int, stream_ids, tokens, logits_ptr, next_ptr) -> None:
@@ -248,6 +259,12 @@ class Context:
         hh_prefill(self.ctx, stream_id, tokens, mode, None if buf is None else buf.ctypes.data,
                    nxt.ctypes.data)
         return int(nxt[0]), buf
+
+    def prefill_batch(self, stream_ids, prompts) -> np.ndarray:
+        """Prompts of several streams in one pass; returns their next tokens."""
+        nxt = np.zeros(len(stream_ids), dtype=np.int32)
+        hh_prefill_batch(self.ctx, stream_ids, prompts, nxt.ctypes.data)
+        return nxt
 
     def decode_step(self, stream_ids=None, tokens=None, logits: bool = False, n_streams: int | None = None,
                     host_next: bool = True):

@@ -146,8 +146,9 @@ class Server:
         return a
 
     def answer_batch(self, queries: Sequence[str], n_tokens: int, streams: Sequence[int]) -> List[Answer]:
-        """Serve several queries at once: each routed query is rendered and
-        prefilled into its own decoder stream (``streams[i]`` for query i),
+        """Serve several queries at once: each routed query is rendered into
+        its own decoder stream (``streams[i]`` for query i), the prompts are
+        prefilled together (passes of the library's multi-stream prefill),
         then all of them decode in lockstep (one multi-stream step per token,
         device-fed), every step's tokens copied behind one event.  Escalated
         queries take no stream time.  Clocks run from the batch's arrival."""
@@ -166,15 +167,28 @@ class Server:
             out.append(a)
             if not esc:
                 live.append(i)
+        prompts = {}
         for i in live:
             a = out[i]
-            ids = byte_tokens(hh.hh_render_marker(self.answers[a.entry]))
-            a.prompt_tokens = len(ids)
+            prompts[i] = byte_tokens(hh.hh_render_marker(self.answers[a.entry]))
+            a.prompt_tokens = len(prompts[i])
             a.t_render = time.perf_counter() - t0
             self.ctx.reset(streams[i])
-            first, _ = self.ctx.prefill(streams[i], ids)
-            a.t_first = time.perf_counter() - t0
-            a.tokens.append(first)
+        # Prompts in passes of at most one prefill pass's rows each.
+        cfg = self.ctx.cfg
+        cap = max(min(cfg.max_prefill or cfg.max_context, cfg.max_context), cfg.max_streams)
+        group: List[int] = []
+        for k, i in enumerate(live):
+            group.append(i)
+            rows = sum(len(prompts[j]) for j in group)
+            nxt_rows = len(prompts[live[k + 1]]) if k + 1 < len(live) else None
+            if nxt_rows is None or rows + nxt_rows > cap:
+                firsts = self.ctx.prefill_batch([streams[j] for j in group], [prompts[j] for j in group])
+                now = time.perf_counter() - t0
+                for j, f in zip(group, firsts):
+                    out[j].t_first = now
+                    out[j].tokens.append(int(f))
+                group = []
         n = len(live)
         if n == 0 or n_tokens == 1:
             for i in live:
