@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import check_logits, new_context
+from gpu_util import check_logits, new_context, top2_margin
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -128,3 +128,27 @@ def test_multistream_lockstep(one_b, ctx):
         ref = model.decode_batch(caches, feed)
         worst = max(worst, check_logits(lg, ref, TOL, what=f"multi step {step}"))
     print(f"1B 4-stream decode: max-abs {worst:.4g}")
+
+
+def test_prefill_batch_1b(one_b, ctx):
+    """Three ragged prompts in one hh_prefill_batch pass on the 1B bf16 model
+    (MFMA GEMMs over the packed rows, per-row attention, n-row head): next
+    tokens and the KV each stream is left with, checked by a lockstep decode
+    step, against the oracle's run of each stream alone."""
+    shape, _, model = one_b
+    ctx.reset()
+    ids = [4, 1, 2]
+    prompts = [synth.make_tokens(shape.vocab, n, 400 + n) for n in (77, 5, 40)]
+    nxt = ctx.prefill_batch(ids, prompts)
+    caches, worst = [], 0.0
+    for k, p in enumerate(prompts):
+        logits, cache = model.prefill(p, rows="last")
+        caches.append(cache)
+        if top2_margin(logits[0]) > 1e-2:
+            assert int(nxt[k]) == int(np.argmax(logits[0])), f"stream {ids[k]}"
+    feed = np.array([101, 202, 303], dtype=np.int32)
+    _, lg = ctx.decode_step(ids, feed, logits=True)
+    for k in range(3):
+        worst = max(worst, check_logits(lg[k], model.decode(caches[k], int(feed[k])), TOL,
+                                        what=f"1B batch prefill stream {ids[k]}"))
+    print(f"1B batch prefill (77, 5, 40 rows) then lockstep step: max-abs {worst:.4g}")
