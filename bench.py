@@ -11,8 +11,10 @@ because a dense decoder's cost depends only on lengths.
 Printed: ONE JSON line with decode tok/s (value), TTFT, the HBM roofline of
 the persistent decode-step kernel (one launch per token, timed with HIP events
 on the library's stream) and the fp64 CPU oracle timed on a bounded sample.
-With --other-configs it adds context figures for the three other 1B workloads
-(1024-token prompt TTFT, 8192-token cache decode, 32 lockstep streams).
+The same line carries the three other 1B workloads, measured on the same
+context: the 1024-token prompt's TTFT and its MFMA fraction (device time of
+the prefill against the dense fp16 peak), decode over 8192 cached positions
+and 32 lockstep streams, each with its HBM fraction.
 """
 from __future__ import annotations
 
@@ -29,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_FLOPS = 2.5166e15  # dense fp16/bf16: 256 CUs x 2.4 GHz x 4096 FLOP per clock
 METRIC = "batch-1 decode tok/s + % HBM roofline; TTFT (ms) for 1B bf16 model"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_step_1b_traffic.json")
 STEP_SOURCES = ["paper_2606_12154_amd/csrc/k_step.hip", "paper_2606_12154_amd/csrc/hh_device.h",
@@ -69,8 +72,9 @@ def measured_traffic(launch_bytes: float):
 
 
 def cpu_baseline(shape, wseed, prompt, n_decode):
-    """The fp64 oracle on the host: prefill of the prompt, then n_decode
-    cached decode steps; returns (decode tok/s, prefill seconds, threads)."""
+    """The oracle on the host, in its fp64 working precision and again in
+    fp32: prefill of the prompt, then n_decode cached decode steps.  Returns
+    {precision: (decode tok/s, prefill seconds)} and the threads used."""
     import oracle
     import synth
     try:
@@ -78,17 +82,30 @@ def cpu_baseline(shape, wseed, prompt, n_decode):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count() or 1
-    tensors = synth.make_weights(shape, wseed)
-    model = oracle.Decoder(shape, synth.weights_as_f64(shape, tensors))
-    del tensors
-    t0 = time.perf_counter()
-    logits, cache = model.prefill(prompt, rows="last")
-    t1 = time.perf_counter()
-    tok = int(np.argmax(logits[0]))
-    for _ in range(n_decode):
-        tok = int(np.argmax(model.decode(cache, tok)))
-    t2 = time.perf_counter()
-    return n_decode / (t2 - t1), t1 - t0, cores
+    w64 = synth.weights_as_f64(shape, synth.make_weights(shape, wseed))
+    out = {}
+    for name, dt in (("fp64", np.float64), ("fp32", np.float32)):
+        model = oracle.Decoder(shape, w64, dtype=dt)
+        t0 = time.perf_counter()
+        logits, cache = model.prefill(prompt, rows="last")
+        t1 = time.perf_counter()
+        tok = int(np.argmax(logits[0]))
+        for _ in range(n_decode):
+            tok = int(np.argmax(model.decode(cache, tok)))
+        t2 = time.perf_counter()
+        out[name] = (n_decode / (t2 - t1), t1 - t0)
+        del model, cache
+    return out, cores
+
+
+def prefill_flops(shape, P: int) -> float:
+    """Algorithmic FLOPs of a P-token prompt evaluation: every projection of
+    every row (2 per weight), causal attention (Q K^T and P V over the
+    P (P + 1) / 2 visible pairs of every head) and the LM head of the last row."""
+    d, hd = shape.d_model, shape.head_dim
+    lin = shape.n_layers * (d * (shape.q_dim + 2 * shape.kv_dim) + shape.q_dim * d + 3 * d * shape.ffn_dim)
+    attn = shape.n_layers * shape.n_heads * 4 * hd * P * (P + 1) / 2
+    return 2.0 * lin * P + attn + 2.0 * shape.vocab * d
 
 
 def measure_others(ctx, shape, st, names):
@@ -102,24 +119,37 @@ def measure_others(ctx, shape, st, names):
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     if "prompt1024" in names:
-        # 1024-token prompt: TTFT (the prefill-dominated workload), then 64 steps.
+        # 1024-token prompt: TTFT (the prefill-dominated workload), then 64
+        # steps.  TTFT is host to host (token ids in, first id out); the
+        # MFMA fraction uses the prefill's device time (events on the
+        # library's stream around the same call).
         w3 = synth.WORKLOADS["1b_prefill"]
         p3 = synth.make_tokens(shape.vocab, w3["prompt"], w3["tseed"])
-        tt = []
-        for i in range(4):
+        tt, dev = [], []
+        for i in range(6):
             ctx.reset(0)
+            torch.cuda.synchronize()
             t0 = time.perf_counter()
+            e0.record(st)
             ctx.prefill(0, p3)
+            e1.record(st)
+            t1 = time.perf_counter()
+            e1.synchronize()
             if i:
-                tt.append(time.perf_counter() - t0)
+                tt.append(t1 - t0)
+                dev.append(e0.elapsed_time(e1) / 1e3)
         e0.record(st)
         for _ in range(w3["steps"]):
             hh.hh_decode_step(ctx.ctx, 1, None, None, None, None)
         e1.record(st)
         e1.synchronize()
+        fl = prefill_flops(shape, w3["prompt"])
         other["prompt1024"] = {"ttft_ms": round(float(np.mean(tt)) * 1e3, 3),
                                "ttft_ms_min": round(float(np.min(tt)) * 1e3, 3),
-                               "prefill_tflops": round(2.062e12 / float(np.mean(tt)) / 1e12, 1),
+                               "prefill_device_ms": round(float(np.mean(dev)) * 1e3, 3),
+                               "prefill_flop": fl,
+                               "prefill_tflops": round(fl / float(np.mean(dev)) / 1e12, 1),
+                               "mfma_frac": round(fl / float(np.mean(dev)) / MFMA_PEAK_FLOPS, 4),
                                "decode_tok_s": round(w3["steps"] / (e0.elapsed_time(e1) / 1e3), 1)}
 
     if "cache8192" in names:
@@ -136,6 +166,8 @@ def measure_others(ctx, shape, st, names):
         t4 = w4["prompt"] + (w4["steps"] - 1) / 2.0 + 1
         b4 = decode_step_bytes(shape, t4)
         other["cache8192"] = {"decode_tok_s": round(w4["steps"] / s4, 1),
+                              "ms_per_token": round(s4 / w4["steps"] * 1e3, 4),
+                              "bytes_per_token": int(b4),
                               "hbm_frac": round(b4 * w4["steps"] / s4 / 1e9 / HBM_PEAK_GBS, 4)}
 
     if "streams32" in names:
@@ -156,6 +188,7 @@ def measure_others(ctx, shape, st, names):
         t5 = w5["prompt"] + 1 + n5 / 2.0 + 1
         b5 = shape.n_params() * 2 + ns * kv_bytes_per_position(shape) * (t5 + 1)
         other["streams32"] = {"aggregate_tok_s": round(ns * n5 / s5, 1), "step_ms": round(s5 / n5 * 1e3, 3),
+                              "bytes_per_step": int(b5),
                               "hbm_frac": round(b5 * n5 / s5 / 1e9 / HBM_PEAK_GBS, 4)}
     return other
 
@@ -363,8 +396,8 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--other-configs", action="store_true",
-                    help="also measure the 1024-token prompt, 8192-token cache and 32-stream workloads")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the 1024-token prompt, 8192-token cache and 32-stream workloads")
     ap.add_argument("--only", choices=["prompt1024", "cache8192", "streams32", "ctxsweep", "windows", "q4decode",
                                        "e2e"],
                     help="measure just this one of the other workloads (for a kernel trace of it); "
@@ -506,18 +539,32 @@ def main():
                      "frac_of_measured_read": round(achieved / read_gbs, 4)},
     }
 
-    if args.other_configs:
-        out["other_configs"] = measure_others(ctx, shape, st, ["prompt1024", "cache8192", "streams32"])
+    if not args.no_other_configs:
+        # The other workloads on the same context, as keys of the same line.
+        oth = measure_others(ctx, shape, st, ["prompt1024", "cache8192", "streams32"])
+        a, b, c = oth["prompt1024"], oth["cache8192"], oth["streams32"]
+        out.update({
+            "ttft_ms_p1024": a["ttft_ms"], "ttft_ms_p1024_min": a["ttft_ms_min"],
+            "prefill_p1024_device_ms": a["prefill_device_ms"], "prefill_p1024_tflops": a["prefill_tflops"],
+            "prefill_mfma_frac": a["mfma_frac"], "decode_tok_s_p1024": a["decode_tok_s"],
+            "cache8192_decode_tok_s": b["decode_tok_s"], "cache8192_ms_per_token": b["ms_per_token"],
+            "cache8192_hbm_frac": b["hbm_frac"],
+            "streams32_tok_s": c["aggregate_tok_s"], "streams32_step_ms": c["step_ms"],
+            "streams32_hbm_frac": c["hbm_frac"],
+        })
 
     ctx.close()
     del ctx
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        rate, pre_s, cores = cpu_baseline(shape, wl["wseed"], prompt, args.cpu_decode_steps)
+        res, cores = cpu_baseline(shape, wl["wseed"], prompt, args.cpu_decode_steps)
+        (rate, pre_s), (rate32, pre32) = res["fp64"], res["fp32"]
         out["cpu_baseline"] = {"value": round(rate, 4), "unit": "tok/s", "cores": cores, "kind": "oracle",
-                               "sample": f"fp64 numpy oracle on the same weights: prefill of the {P}-token prompt "
-                                         f"({pre_s:.1f} s, not in the rate), then {args.cpu_decode_steps} cached "
-                                         f"decode steps (rate = steps / their wall time)"}
+                               "sample": f"the numpy oracle (fp64) on the same weights: prefill of the {P}-token "
+                                         f"prompt ({pre_s:.1f} s, not in the rate), then {args.cpu_decode_steps} "
+                                         f"cached decode steps (rate = steps / their wall time)",
+                               "fp32": {"value": round(rate32, 4), "unit": "tok/s", "prefill_s": round(pre32, 2),
+                                        "sample": "the same oracle and request in fp32 working precision"}}
     print(json.dumps(out), flush=True)
 
 

@@ -133,21 +133,22 @@ hh_status hh_prefill(hh_ctx* ctx, int32_t stream_id, const int32_t* tokens, int3
                      int32_t logits_mode, float* logits, int32_t* next_token);
 
 /*
- * Prompt evaluation for several streams in one pass (several requests
+ * Prompt evaluation for several streams together (several requests
  * arriving together, the paper's runtime phase at more than one user): the
  * prompts of n distinct streams are appended as one set of rows, every layer
- * runs once over all of them (each row attends to its own stream's keys up
- * to its position), and the greedy next token of each stream comes from its
- * last row, as hh_prefill would give it.
+ * runs over all of them (each row attends to its own stream's keys up to its
+ * position), and the greedy next token of each stream comes from its last
+ * row, as hh_prefill would give it.  Rows go through in passes of at most
+ * max_prefill rows (max_context when 0, and at least max_streams), in
+ * stream_ids order; a prompt that does not fit in what is left of a pass
+ * continues in the next one.
  *  stream_ids   host, n distinct ids; lengths host, n counts >= 1.
  *  tokens       host, the prompts concatenated in stream_ids order
- *               (sum of lengths ids in [0, vocab)); the sum must not exceed
- *               the rows of one pass (max_prefill, or max_context when 0,
- *               and at least max_streams).
+ *               (sum of lengths ids in [0, vocab)).
  *  next_tokens  NULL or n int32 (host or device), in stream_ids order.
- * The call waits for its pass to finish.  Errors: INVALID_ARG (n outside
- * 1..max_streams, an id out of range or repeated, a length < 1, too many
- * rows, a token out of range), CONTEXT_FULL, NOT_LOADED, HIP.
+ * The call waits for its passes to finish.  Errors: INVALID_ARG (n outside
+ * 1..max_streams, an id out of range or repeated, a length < 1, a token out
+ * of range), CONTEXT_FULL, NOT_LOADED, HIP.
  */
 hh_status hh_prefill_batch(hh_ctx* ctx, int32_t n, const int32_t* stream_ids, const int32_t* lengths,
                            const int32_t* tokens, int32_t* next_tokens);
@@ -164,11 +165,19 @@ hh_status hh_prefill_batch(hh_ctx* ctx, int32_t n, const int32_t* stream_ids, co
  * A stream with no tokens yet decodes at position 0 (its pending token must
  * then be given through tokens).  Errors: INVALID_ARG, CONTEXT_FULL,
  * NOT_LOADED, HIP.
+ * Failure of a batch-1 step: every cross-workgroup wait of the single-kernel
+ * step is bounded (about 1 s).  When one gives up, the step's token is -1
+ * (pending token, next_tokens, and the history hh_read_argmax returns), and
+ * so is the token of every later step of that stream, and of every step of
+ * any stream until hh_reset; the first call with host outputs after the
+ * failure returns HH_ERR_HIP.  Device-fed loops detect it by the -1.
  */
 hh_status hh_decode_step(hh_ctx* ctx, int32_t n_streams, const int32_t* stream_ids,
                          const int32_t* tokens, float* logits, int32_t* next_tokens);
 
-/* Drop a stream's KV pages and set its length to 0 (stream_id -1: all). */
+/* Drop a stream's KV pages and set its length to 0 (stream_id -1: all).
+ * Also clears the context's record of a failed decode step (see
+ * hh_decode_step). */
 hh_status hh_reset(hh_ctx* ctx, int32_t stream_id);
 
 /* Current length (positions held in the KV cache) of a stream. */

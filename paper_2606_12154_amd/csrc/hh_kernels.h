@@ -11,7 +11,8 @@ namespace hh {
 template <typename TW, typename TKV, typename TM>
 struct DecodeKernels {
   static void prep_embed(hipStream_t st, int n_rows, int prefill_stream, const int* feed, int* row_stream,
-                         int* row_pos, const int* pos, const int* pending, const TW* embed, float* x, int d);
+                         int* row_pos, const int* pos, const int* pending, unsigned long long* slot, const TW* embed,
+                         float* x, int d);
   static void qkv_gemv(hipStream_t st, const TW* W, const float* x, const float* gain, float eps, int d, int hq,
                        int hkv, const int* row_stream, const int* row_pos, const float2* rope, float* q, TKV* kv,
                        KvLayout L, int layer, const int* page_table);
@@ -100,6 +101,8 @@ struct StepParams {
   int load_depth;              // ring slots each streaming wave keeps in flight (1 .. 7)
   int quiet;                   // 1: streaming pauses while compute waves wait for other workgroups
   int poll_delay;              // ticks (10 ns) to wait before a phase's first exchange poll
+  unsigned long long wait_ticks;  // ticks (10 ns) after which a wait gives up (0: 1 s)
+  int fail_wait;               // tests of the failure path: the final argmax wait expects an epoch never published
   float eps;
   unsigned epoch;              // base epoch of this step (distinct for every step)
   const LayerPtrs<TW>* layer;  // device array [n_layers]

@@ -23,16 +23,24 @@ template <typename TW>
 __global__ __launch_bounds__(256) void k_prep_embed(int prefill_stream, const int* __restrict__ feed,
                                                     int* __restrict__ row_stream, int* __restrict__ row_pos,
                                                     const int* __restrict__ pos, const int* __restrict__ pending,
+                                                    unsigned long long* __restrict__ slot,
                                                     const TW* __restrict__ embed, float* __restrict__ x, int d) {
   // prefill_stream >= 0: rows r of that stream at positions pos + r; -1: one
   // row per listed stream at its position; -2: row_stream and row_pos given.
   const int r = blockIdx.x;
   const int s = prefill_stream >= 0 ? prefill_stream : row_stream[r];
   const int p = prefill_stream == -2 ? row_pos[r] : pos[s] + (prefill_stream >= 0 ? r : 0);
-  const int tok = feed ? feed[r] : pending[s];
+  int tok = feed ? feed[r] : pending[s];
   if (threadIdx.x == 0 && prefill_stream != -2) {
     row_pos[r] = p;
     if (prefill_stream >= 0) row_stream[r] = s;
+  }
+  // A negative pending token marks a stream whose earlier decode step gave
+  // up (see k_finalize): the row gathers row 0 and its argmax slot is pinned
+  // to the all-ones key, which k_finalize turns back into -1.
+  if (tok < 0) {
+    tok = 0;
+    if (threadIdx.x == 0) slot[s] = ~0ull;
   }
   const TW* e = embed + (size_t)tok * d;
   for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)r * d + i] = (float)e[i];
@@ -49,7 +57,8 @@ __global__ void k_finalize(int r0, int n, const int* __restrict__ row_stream, co
     const int s = row_stream[r];
     const int p = row_pos[r];
     if (slot) {
-      const int tok = argmax_index(slot[s]);
+      const unsigned long long key = slot[s];
+      const int tok = key == ~0ull ? -1 : argmax_index(key);
       pending[s] = tok;
       hist[(size_t)s * max_ctx + p] = tok;
       slot[s] = 0ull;
@@ -613,8 +622,9 @@ __global__ __launch_bounds__(256) void k_rmsnorm_rows(const float* __restrict__ 
 template <typename TW, typename TKV, typename TM>
 void DecodeKernels<TW, TKV, TM>::prep_embed(hipStream_t st, int n_rows, int prefill_stream, const int* feed,
                                             int* row_stream, int* row_pos, const int* pos, const int* pending,
-                                            const TW* embed, float* x, int d) {
-  k_prep_embed<TW><<<n_rows, 256, 0, st>>>(prefill_stream, feed, row_stream, row_pos, pos, pending, embed, x, d);
+                                            unsigned long long* slot, const TW* embed, float* x, int d) {
+  k_prep_embed<TW><<<n_rows, 256, 0, st>>>(prefill_stream, feed, row_stream, row_pos, pos, pending, slot, embed, x,
+                                           d);
 }
 
 template <typename TW, typename TKV, typename TM>

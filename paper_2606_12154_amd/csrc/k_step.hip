@@ -11,19 +11,21 @@
 // computed by all CUs.  The kernel therefore separates streaming from
 // computing inside each workgroup:
 //
-//  * wave 0 (the streaming wave) walks the workgroup's whole byte stream for
-//    the token -- its rows of every weight matrix, layer by layer, plus the
-//    K/V pages of its attention item -- and copies it with direct global->LDS
-//    loads into a ring of 8 KiB slots.  It keeps only a few slots in flight
-//    (enough to saturate HBM, few enough that the memory queues stay short),
-//    and it never waits for activations: it only waits for free ring slots.
-//  * waves 1..7 (compute waves) wait for a phase's input vector, then consume
-//    the phase's ring slots (dot products of staged rows with the input, or
-//    attention over staged K/V pages), and publish the phase's outputs.
+//  * waves 0..2 (the streaming waves) walk the workgroup's whole byte stream
+//    for the token -- its rows of every weight matrix, layer by layer, plus
+//    the K/V pages of its attention item -- and copy it with direct
+//    global->LDS loads into a ring of 8 KiB slots (slot n by wave n % 3).
+//    Each keeps only a few slots in flight (together enough to saturate HBM,
+//    few enough that the memory queues stay short), and none waits for
+//    activations: they only wait for free ring slots.
+//  * waves 3..7 (the five compute waves) wait for a phase's input vector,
+//    then consume the phase's ring slots (dot products of staged rows with
+//    the input, or attention over staged K/V pages), and publish the phase's
+//    outputs.
 //
 // While compute waves wait for other CUs at a phase boundary, the streaming
-// wave keeps filling the ring with the next phases' weights, so HBM stays busy
-// through the exchange latency instead of idling.
+// waves keep filling the ring with the next phases' weights, so HBM stays
+// busy through the exchange latency instead of idling.
 //
 // Workgroups exchange activations without grid barriers or memory fences:
 // every value crossing workgroups travels as one 64-bit word (fp32 bits | a
@@ -92,6 +94,7 @@ __host__ __device__ constexpr int step_xc_floats(int d, int hq, int hkv) {
 
 // LDS block shared by the streaming and compute waves.
 struct RingSync {
+  unsigned long long wait_ticks;  // a wait gives up after this many ticks of the 100 MHz clock
   int cbar;      // arrivals at compute-wave barriers
   int abort;     // set when a wait gave up: every later wait returns at once
   int quiet;     // compute waves are waiting for another workgroup's outputs
@@ -100,8 +103,9 @@ struct RingSync {
   float ss[kNC];           // per compute wave: partial sum of squares of a staged vector
 };
 
-// Called in a wait loop: true once the wait must give up (after 1 s, or once
-// any wait of this workgroup or of another one has given up).
+// Called in a wait loop: true once the wait must give up (after wait_ticks,
+// 1 s unless the host sets a shorter limit, or once any wait of this
+// workgroup or of another one has given up).
 __device__ __forceinline__ bool give_up(unsigned& spins, unsigned long long& t0, RingSync HH_LDS* sy, int HH_GLB* err) {
   if ((++spins & 63u) != 0) return false;
   if (*(volatile int HH_LDS*)&sy->abort) return true;
@@ -110,7 +114,7 @@ __device__ __forceinline__ bool give_up(unsigned& spins, unsigned long long& t0,
     t0 = t;
     return false;
   }
-  if (t - t0 > kWaitTicks || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+  if (t - t0 > sy->wait_ticks || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
     *(volatile int HH_LDS*)&sy->abort = 1;
     __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return true;
@@ -649,6 +653,22 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
   const int t = p + 1;  // keys attended this step
   const unsigned E0 = P.epoch;
   const int s_cap = nwg / hkv;
+  // A step whose input is the -1 left by an abandoned step, or that starts
+  // after a wait of this context gave up, computes nothing: the stream
+  // records -1 at this position and moves on, so device-fed consumers see
+  // the failure instead of a plausible token.
+  // (One thread decides, so the whole workgroup takes the same branch.)
+  __shared__ int dead;
+  if (tid == 0) dead = tok < 0 || __hip_atomic_load((int*)P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+  __syncthreads();
+  if (dead) {
+    if (wg == 0 && tid == 0) {
+      P.pending[s] = -1;
+      P.hist[(size_t)s * P.max_ctx + p] = -1;
+      P.pos[s] = p + 1;
+    }
+    return;
+  }
 
   char* ring = smem;
   float* xa = reinterpret_cast<float*>(smem + (size_t)S * kSlot);  // [d] normalised inputs (QKV, GU, head)
@@ -666,6 +686,7 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
     syp->landed[tid] = tid - S;
   }
   if (tid == 0) {
+    syp->wait_ticks = P.wait_ticks > 0 ? P.wait_ticks : kWaitTicks;
     syp->quiet = 0;
     syp->cbar = 0;
     syp->abort = 0;
@@ -1547,20 +1568,23 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
       ll_put_u(P.ll_keys + 2 * wg + 1, (unsigned)best, e6);
     }
     if (wg == 0) {
+      // fail_wait (a test of the failure path, set from the host): wait for
+      // an epoch no workgroup publishes, so this wait runs into its limit.
+      const unsigned e6w = P.fail_wait ? E0 + 511u : e6;
       unsigned long long b = 0ull;
       for (int i0 = 0; i0 < nwg; i0 += 64) {
         const int i = i0 + lane;
-        unsigned long long hi = (unsigned long long)e6 << 32, lo = hi;
+        unsigned long long hi = (unsigned long long)e6w << 32, lo = hi;
         if (i < nwg) {
           hi = ll_get(P.ll_keys + 2 * i);
           lo = ll_get(P.ll_keys + 2 * i + 1);
         }
         unsigned spins = 0;
         unsigned long long t0 = 0;
-        while (__any((unsigned)(hi >> 32) != e6 || (unsigned)(lo >> 32) != e6)) {
+        while (__any((unsigned)(hi >> 32) != e6w || (unsigned)(lo >> 32) != e6w)) {
           __builtin_amdgcn_s_sleep(1);
-          if ((unsigned)(hi >> 32) != e6) hi = ll_get(P.ll_keys + 2 * i);
-          if ((unsigned)(lo >> 32) != e6) lo = ll_get(P.ll_keys + 2 * i + 1);
+          if ((unsigned)(hi >> 32) != e6w) hi = ll_get(P.ll_keys + 2 * i);
+          if ((unsigned)(lo >> 32) != e6w) lo = ll_get(P.ll_keys + 2 * i + 1);
           if (give_up(spins, t0, syp, err)) break;
         }
         if (i < nwg) {
@@ -1574,7 +1598,9 @@ __global__ __launch_bounds__(kStepThreads) void k_decode_step(StepParams<TW, TKV
         b = o2 > b ? o2 : b;
       }
       if (lane == 0) {
-        const int nt = argmax_index(b);
+        // A wait of this step gave up: its argmax is not a result.
+        const bool gave_up = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+        const int nt = gave_up ? -1 : argmax_index(b);
         P.pending[s] = nt;
         P.hist[(size_t)s * P.max_ctx + p] = nt;
         P.pos[s] = p + 1;

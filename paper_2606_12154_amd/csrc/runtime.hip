@@ -79,6 +79,26 @@ bool config_supported(const hh_config& c, std::string& why) {
   return true;
 }
 
+// Where the decode-step kernel's exchange words live: the context's arena
+// (the default), or another buffer of the same layout.
+// Layout for up to `cap` workgroups: xa, xb [d], q [Hq*64], kn, vn
+// [Hkv*64], attention partials [Hq][cap][66], o [Hq*64], down partials
+// [cap][d], argmax keys [2*cap], then the error word.
+struct StepWords {
+  unsigned long long* base;
+  size_t cap;
+  unsigned epoch;  // first epoch of this step (a multiple of 512, never 0)
+};
+
+size_t step_words(const hh_config& g, size_t cap) {
+  const size_t d = g.d_model, hq = g.n_heads, hkv = g.n_kv_heads;
+  return 2 * d + 2 * hq * 64 + 2 * hkv * 64 + hq * cap * 66 + cap * d + 2 * cap + 8;
+}
+
+int* step_err_word(const hh_config& g, const StepWords& w) {
+  return reinterpret_cast<int*>(w.base + step_words(g, w.cap) - 8);
+}
+
 Layout make_layout(const hh_config& c) {
   Layout L{};
   const bool bf = c.dtype == HH_BF16;
@@ -156,8 +176,7 @@ Layout make_layout(const hh_config& c) {
   // xa, xb [d], q [Hq*64], kn, vn [Hkv*64], partials [Hq][kMaxStepWG][66],
   // o [Hq*64], down partials [kMaxStepWG][d], keys [2*kMaxStepWG], then the
   // error flag.
-  L.ll_words = 2 * d + 2 * (size_t)hq * 64 + 2 * (size_t)c.n_kv_heads * 64 + (size_t)hq * kMaxStepWG * 66 +
-               (size_t)kMaxStepWG * d + 2 * kMaxStepWG + 8;
+  L.ll_words = step_words(c, kMaxStepWG);
   L.ll = take(L.ll_words * 8);
   L.layer_tab = take((size_t)c.n_layers * sizeof(LayerPtrs<float>));
   L.trace = take((size_t)kMaxStepWG * (c.n_layers + 1) * 32 * 8);  // optional phase timestamps
@@ -209,6 +228,9 @@ struct hh_ctx {
   int step_quiet = 0;               // HH_STEP_QUIET: pause streaming during exchange waits
   int step_ring = kStepRingSlots;   // HH_RING_SLOTS: LDS ring slots used (at most kStepRingSlots)
   int step_poll_delay = 60;         // HH_POLL_DELAY: 10 ns ticks before a phase's first exchange poll
+  unsigned long long step_wait_ticks = 0;  // HH_STEP_WAIT_TICKS: wait limit (10 ns ticks; 0: 1 s), and
+  int step_fail_wait = 0;                  // HH_STEP_FAIL_WAIT: one wait that never completes -- both for
+                                           // tests of the failure path
   std::string trace_path;   // HH_STEP_TRACE: file receiving the last traced step's phase timestamps
   std::string err;
   // host mirror of the device bookkeeping
@@ -334,8 +356,8 @@ void enqueue_decode(hh_ctx* c, int n, bool feed, bool want_logits) {
   const Layout& L = c->L;
   using DK = DecodeKernels<TW, TKV, TM>;
   DK::prep_embed(c->stream, n, -1, feed ? c->at<int>(L.feed) : nullptr, c->at<int>(L.row_stream),
-                 c->at<int>(L.row_pos), c->at<int>(L.pos), c->at<int>(L.pending), c->at<TW>(L.embed),
-                 c->at<float>(L.x), c->cfg.d_model);
+                 c->at<int>(L.row_pos), c->at<int>(L.pos), c->at<int>(L.pending),
+                 c->at<unsigned long long>(L.slot), c->at<TW>(L.embed), c->at<float>(L.x), c->cfg.d_model);
   // The batch-1 GEMV kernels read the model's own (bf16) matrices, which a
   // 4-bit model does not compute with: it takes the MFMA path at one row.
   const bool gemv = n == 1 && c->cfg.weight_format == HH_WF_DTYPE;
@@ -414,7 +436,7 @@ hipError_t setup_step_kernel(hh_ctx* c) {
 }
 
 template <typename TW, typename TKV>
-hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
+hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits, const StepWords& words) {
   const hh_config& g = c->cfg;
   const Layout& L = c->L;
   StepParams<TW, TKV> P{};
@@ -430,11 +452,10 @@ hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
   P.load_depth = c->step_depth;
   P.quiet = c->step_quiet;
   P.poll_delay = c->step_poll_delay;
+  P.wait_ticks = c->step_wait_ticks;
+  P.fail_wait = c->step_fail_wait;
   P.eps = g.rms_eps;
-  // Each step owns 512 epochs (8 phases x 64 layers); epoch 0 is never used,
-  // so the zero-initialised exchange words never look current.
-  c->step_count += 1;
-  P.epoch = c->step_count * 512u;
+  P.epoch = words.epoch;
   P.layer = c->at<LayerPtrs<TW>>(L.layer_tab);
   P.embed = c->at<typename StepEmbed<TW>::type>(L.embed);
   // 4-bit rows carry their own scales (no power-of-two factor).
@@ -451,18 +472,18 @@ hh_status launch_step(hh_ctx* c, int s, bool feed, bool want_logits) {
   P.hist = c->at<int>(L.hist);
   P.feed = feed ? c->at<int>(L.feed) : nullptr;
   P.logits = want_logits ? c->at<float>(L.logits) : nullptr;
-  unsigned long long* w = c->at<unsigned long long>(L.ll);
-  const size_t d = g.d_model, hq = g.n_heads, hkv = g.n_kv_heads;
+  unsigned long long* w = words.base;
+  const size_t d = g.d_model, hq = g.n_heads, hkv = g.n_kv_heads, cap = words.cap;
   P.ll_xa = w;
   P.ll_xb = P.ll_xa + d;
   P.ll_q = P.ll_xb + d;
   P.ll_kn = P.ll_q + hq * 64;
   P.ll_vn = P.ll_kn + hkv * 64;
   P.ll_part = P.ll_vn + hkv * 64;
-  P.ll_o = P.ll_part + hq * kMaxStepWG * 66;
+  P.ll_o = P.ll_part + hq * cap * 66;
   P.ll_dp = P.ll_o + hq * 64;
-  P.ll_keys = P.ll_dp + (size_t)kMaxStepWG * d;
-  P.err = reinterpret_cast<int*>(P.ll_keys + 2 * kMaxStepWG);
+  P.ll_keys = P.ll_dp + cap * d;
+  P.err = reinterpret_cast<int*>(P.ll_keys + 2 * cap);
   P.trace = c->trace_path.empty() ? nullptr : c->at<unsigned long long>(L.trace);
   const hipError_t e = StepKernel<TW, TKV>::launch(P, c->step_wg, c->stream);
   if (e != hipSuccess) return c->hip_fail(e, "decode-step kernel launch");
@@ -528,7 +549,8 @@ hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, f
     const bool last = r0 + P == n;
     HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens + r0, P * sizeof(int), hipMemcpyHostToDevice, st));
     DK::prep_embed(st, P, s, c->at<int>(L.feed), c->at<int>(L.row_stream), c->at<int>(L.row_pos), c->at<int>(L.pos),
-                   c->at<int>(L.pending), c->at<TW>(L.embed), c->at<float>(L.x), c->cfg.d_model);
+                   c->at<int>(L.pending), c->at<unsigned long long>(L.slot), c->at<TW>(L.embed), c->at<float>(L.x),
+                   c->cfg.d_model);
     enqueue_layers<TW, TKV, TM>(c, P, false, 1, -2, nullptr, s, c->len[s] + r0);
     unsigned long long* slot = c->at<unsigned long long>(L.slot);
     if (mode == HH_LOGITS_ALL) {
@@ -553,9 +575,12 @@ hh_status do_prefill(hh_ctx* c, int s, const int32_t* tokens, int n, int mode, f
   return HH_OK;
 }
 
-// Prompts of several streams in one pass: the rows of all of them through
-// every layer (attention per row over its own stream's keys), then the head
-// on the last row of each.
+// Prompts of several streams: their rows go through every layer together
+// (each row attends to its own stream's keys), in passes of at most rows_cap
+// rows; a prompt longer than what is left of a pass continues in the next
+// one (its later rows attend to the keys the earlier pass wrote).  After each
+// pass, the streams whose last row it held get their next token from the
+// n-row head on those rows.
 template <typename TW, typename TKV, typename TM>
 hh_status do_prefill_batch(hh_ctx* c, int n, const int32_t* ids, const int32_t* lens, const int32_t* tokens,
                            int32_t* next) {
@@ -569,58 +594,76 @@ hh_status do_prefill_batch(hh_ctx* c, int n, const int32_t* ids, const int32_t* 
     hh_status rc = ensure_pages(c, ids[i], c->len[ids[i]] + lens[i]);
     if (rc != HH_OK) return rc;
   }
-  std::vector<int> rs, rp, last_s(n), last_p(n), last_r(n);
-  for (int i = 0; i < n; ++i) {
-    for (int j = 0; j < lens[i]; ++j) {
-      rs.push_back(ids[i]);
-      rp.push_back(c->len[ids[i]] + j);
-    }
-    last_r[i] = (int)rs.size() - 1;
-    last_s[i] = ids[i];
-    last_p[i] = rp.back();
-  }
-  const int R = (int)rs.size();
   c->uploaded_streams.clear();
   int* row_stream = c->at<int>(L.row_stream);
   int* row_pos = c->at<int>(L.row_pos);
-  HIPCHK(c, hipMemcpyAsync(row_stream, rs.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
-  HIPCHK(c, hipMemcpyAsync(row_pos, rp.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
-  HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, R * sizeof(int), hipMemcpyHostToDevice, st));
   float* x = c->at<float>(L.x);
-  DK::prep_embed(st, R, -2, c->at<int>(L.feed), row_stream, row_pos, c->at<int>(L.pos), c->at<int>(L.pending),
-                 c->at<TW>(L.embed), x, d);
-  enqueue_layers<TW, TKV, TM>(c, R, false, 1, -2, nullptr);
-  // Last rows to rows 0 .. n-1 (row i's source lies at or after row i and
-  // after every earlier destination), then the n-row head and argmax.
-  for (int i = 0; i < n; ++i)
-    if (last_r[i] != i)
-      HIPCHK(c, hipMemcpyAsync(x + (size_t)i * d, x + (size_t)last_r[i] * d, d * sizeof(float),
-                               hipMemcpyDeviceToDevice, st));
-  HIPCHK(c, hipMemcpyAsync(row_stream, last_s.data(), n * sizeof(int), hipMemcpyHostToDevice, st));
-  HIPCHK(c, hipMemcpyAsync(row_pos, last_p.data(), n * sizeof(int), hipMemcpyHostToDevice, st));
   const float* fn = c->at<float>(L.final_norm);
   unsigned long long* slot = c->at<unsigned long long>(L.slot);
   TM* h = c->at<TM>(L.h);
   const GemmWorkspace gws{c->at<float>(L.gemm_ws), L.gemm_ws_bytes};
-  if (GK::norm_fusable(d)) GK::rmsnorm(st, n, x, d, fn, g.rms_eps, h);
-  else DK::rmsnorm_rows(st, n, x, fn, g.rms_eps, d, h);
-  GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, g.vocab, 1.f / c->wscale, nullptr, slot, row_stream,
-             L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16));
-  finalize(st, 0, n, row_stream, row_pos, slot, c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos),
-           g.max_context);
-  HIPCHK(c, hipGetLastError());
+  std::vector<int> base(n), done(n, 0), offset(n + 1, 0);
+  for (int i = 0; i < n; ++i) {
+    base[i] = c->len[ids[i]];
+    offset[i + 1] = offset[i] + lens[i];
+  }
+  int cur = 0;  // first stream with rows left
+  while (cur < n) {
+    std::vector<int> rs, rp, tk, last_s, last_p, last_r;
+    while (cur < n && (int)rs.size() < L.rows_cap) {
+      const int take = std::min(lens[cur] - done[cur], L.rows_cap - (int)rs.size());
+      for (int j = 0; j < take; ++j) {
+        rs.push_back(ids[cur]);
+        rp.push_back(base[cur] + done[cur] + j);
+        tk.push_back(tokens[offset[cur] + done[cur] + j]);
+      }
+      done[cur] += take;
+      if (done[cur] == lens[cur]) {
+        last_r.push_back((int)rs.size() - 1);
+        last_s.push_back(ids[cur]);
+        last_p.push_back(rp.back());
+        ++cur;
+      }
+    }
+    const int R = (int)rs.size(), ne = (int)last_r.size();
+    HIPCHK(c, hipMemcpyAsync(row_stream, rs.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
+    HIPCHK(c, hipMemcpyAsync(row_pos, rp.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
+    HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tk.data(), R * sizeof(int), hipMemcpyHostToDevice, st));
+    DK::prep_embed(st, R, -2, c->at<int>(L.feed), row_stream, row_pos, c->at<int>(L.pos), c->at<int>(L.pending),
+                   slot, c->at<TW>(L.embed), x, d);
+    enqueue_layers<TW, TKV, TM>(c, R, false, 1, -2, nullptr);
+    if (ne > 0) {
+      // Last rows to rows 0 .. ne-1 (row i's source lies at or after row i
+      // and after every earlier destination), then the head and argmax.
+      for (int i = 0; i < ne; ++i)
+        if (last_r[i] != i)
+          HIPCHK(c, hipMemcpyAsync(x + (size_t)i * d, x + (size_t)last_r[i] * d, d * sizeof(float),
+                                   hipMemcpyDeviceToDevice, st));
+      HIPCHK(c, hipMemcpyAsync(row_stream, last_s.data(), ne * sizeof(int), hipMemcpyHostToDevice, st));
+      HIPCHK(c, hipMemcpyAsync(row_pos, last_p.data(), ne * sizeof(int), hipMemcpyHostToDevice, st));
+      if (GK::norm_fusable(d)) GK::rmsnorm(st, ne, x, d, fn, g.rms_eps, h);
+      else DK::rmsnorm_rows(st, ne, x, fn, g.rms_eps, d, h);
+      GK::logits(st, gws, h, ne, c->at<TM>(L.lm_headM), d, g.vocab, 1.f / c->wscale, nullptr, slot, row_stream,
+                 L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16));
+      finalize(st, 0, ne, row_stream, row_pos, slot, c->at<int>(L.pending), c->at<int>(L.hist), c->at<int>(L.pos),
+               g.max_context);
+    }
+    HIPCHK(c, hipGetLastError());
+    // The host arrays above are read by the copies: wait for them.
+    HIPCHK(c, hipStreamSynchronize(st));
+  }
   if (next)
     for (int i = 0; i < n; ++i)
       HIPCHK(c, hipMemcpyAsync(next + i, c->at<int>(L.pending) + ids[i], sizeof(int), hipMemcpyDefault, st));
-  // The host arrays above are read by the copies: wait for them.
-  HIPCHK(c, hipStreamSynchronize(st));
   for (int i = 0; i < n; ++i) c->len[ids[i]] += lens[i];
   return HH_OK;
 }
 
+// words: null for the context's own exchange words, else the fixed array of
+// the allocation-free entry point (batch-1 single-kernel steps only).
 template <typename TW, typename TKV, typename TM>
 hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t* tokens, float* logits,
-                    int32_t* next) {
+                    int32_t* next, const StepWords* words = nullptr) {
   const Layout& L = c->L;
   hipStream_t st = c->stream;
   for (int i = 0; i < n; ++i) {
@@ -633,13 +676,22 @@ hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t
   }
   if (tokens) HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, n * sizeof(int), hipMemcpyHostToDevice, st));
   const bool want_logits = logits != nullptr;
-  if (n == 1 && c->step_wg > 0) {
+  if (n == 1 && (c->step_wg > 0 || words)) {
+    // Each step owns 512 epochs (8 phases x 64 layers); epoch 0 is never
+    // used, so zero-initialised exchange words never look current.
+    StepWords w{c->at<unsigned long long>(L.ll), (size_t)kMaxStepWG, 0};
+    if (words) {
+      w = *words;
+    } else {
+      c->step_count += 1;
+      w.epoch = c->step_count * 512u;
+    }
     hh_status rc;
     if constexpr (sizeof(TM) == 2)
-      rc = c->step_q4 ? launch_step<Q4Row, TKV>(c, ids[0], tokens != nullptr, want_logits)
-                      : launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits);
+      rc = c->step_q4 ? launch_step<Q4Row, TKV>(c, ids[0], tokens != nullptr, want_logits, w)
+                      : launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits, w);
     else
-      rc = launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits);
+      rc = launch_step<TM, TKV>(c, ids[0], tokens != nullptr, want_logits, w);
     if (rc != HH_OK) return rc;
   } else if (c->use_graphs) {
     auto key = std::make_tuple(n, tokens != nullptr ? 1 : 0, want_logits ? 1 : 0);
@@ -691,14 +743,16 @@ hh_status reset_stream(hh_ctx* c, int s) {
 
 // Synchronize when outputs live in host memory; report a timed-out grid
 // barrier of the persistent decode kernel at that point.
-hh_status finish(hh_ctx* c, bool host_out) {
+hh_status finish(hh_ctx* c, bool host_out, const int* err_word = nullptr) {
   if (!host_out) return HH_OK;
   int err = 0;
-  if (c->step_wg > 0)
-    HIPCHK(c, hipMemcpyAsync(&err, c->at<unsigned long long>(c->L.ll) + c->L.ll_words - 8, sizeof(int),
-                             hipMemcpyDeviceToHost, c->stream));
+  if (!err_word && c->step_wg > 0)
+    err_word = reinterpret_cast<const int*>(c->at<unsigned long long>(c->L.ll) + c->L.ll_words - 8);
+  if (err_word) HIPCHK(c, hipMemcpyAsync(&err, err_word, sizeof(int), hipMemcpyDeviceToHost, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
-  if (err) return c->fail(HH_ERR_HIP, "decode-step exchange wait timed out (workgroups not co-resident)");
+  if (err)
+    return c->fail(HH_ERR_HIP, "decode-step exchange wait timed out (workgroups not co-resident); "
+                               "steps record -1 until hh_reset");
   return HH_OK;
 }
 
@@ -731,6 +785,8 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   if (const char* pd = std::getenv("HH_POLL_DELAY")) c->step_poll_delay = std::max(0, std::atoi(pd));
   if (const char* r = std::getenv("HH_RING_SLOTS")) c->step_ring = std::min(kStepRingSlots, std::max(6, std::atoi(r)));
   if (const char* ld = std::getenv("HH_LOAD_DEPTH")) c->step_depth = std::min(7, std::max(1, std::atoi(ld)));
+  if (const char* wt = std::getenv("HH_STEP_WAIT_TICKS")) c->step_wait_ticks = std::max(1LL, std::atoll(wt));
+  if (const char* fw = std::getenv("HH_STEP_FAIL_WAIT")) c->step_fail_wait = std::atoi(fw) != 0;
   const char* ge = std::getenv("HH_GRAPHS");
   c->use_graphs = !(ge && ge[0] == '0');
   c->len.assign(cfg->max_streams, 0);
@@ -913,7 +969,6 @@ hh_status hh_prefill_batch(hh_ctx* c, int32_t n, const int32_t* stream_ids, cons
       return c->fail(HH_ERR_CONTEXT_FULL, "prompt exceeds max_context");
     total += lengths[i];
   }
-  if (total > c->L.rows_cap) return c->fail(HH_ERR_INVALID_ARG, "prompts exceed the rows of one prefill pass");
   for (long long i = 0; i < total; ++i)
     if (tokens[i] < 0 || tokens[i] >= g.vocab) return c->fail(HH_ERR_INVALID_ARG, "token id out of range");
   hh_status rc = g.dtype == HH_BF16
@@ -962,6 +1017,10 @@ hh_status hh_reset(hh_ctx* c, int32_t s) {
       hh_status rc = reset_stream(c, i);
       if (rc != HH_OK) return rc;
     }
+  // Clear the decode-step kernel's error word: later steps run again (a
+  // stream that recorded -1 keeps it as its pending token until reset).
+  if (c->step_wg > 0)
+    HIPCHK(c, hipMemsetAsync(c->at<unsigned long long>(c->L.ll) + c->L.ll_words - 8, 0, sizeof(int), c->stream));
   return HH_OK;
 }
 

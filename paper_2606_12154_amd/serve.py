@@ -24,6 +24,14 @@ from . import hh
 TAU = 0.05  # margin threshold of the confidence gate (§6.3)
 
 
+def _token(tok: int) -> int:
+    """A streamed id; -1 is the library's mark of a decode step that gave up
+    waiting (the context yields -1 until it is reset)."""
+    if tok < 0:
+        raise RuntimeError("decode step failed (a bounded wait timed out); reset the context")
+    return tok
+
+
 def byte_tokens(prompt: bytes) -> np.ndarray:
     """Stand-in tokenizer: one id per byte, ids 3..258 (0..2 stay free)."""
     return np.frombuffer(prompt, dtype=np.uint8).astype(np.int32) + 3
@@ -121,6 +129,7 @@ class Server:
         a.t_render = time.perf_counter() - t0
         self.ctx.reset(self.stream_id)
         first, _ = self.ctx.prefill(self.stream_id, ids)  # returns once the first token is on the host
+        first = _token(first)
         a.t_first = time.perf_counter() - t0
         a.tokens.append(first)
         yield first
@@ -132,7 +141,7 @@ class Server:
                 self.events[i].record(st)
         for i in range(1, n_tokens):
             self.events[i].synchronize()
-            tok = int(self.host[i, 0])
+            tok = _token(int(self.host[i, 0]))
             a.tokens.append(tok)
             a.t_last = time.perf_counter() - t0
             yield tok
@@ -174,21 +183,14 @@ class Server:
             a.prompt_tokens = len(prompts[i])
             a.t_render = time.perf_counter() - t0
             self.ctx.reset(streams[i])
-        # Prompts in passes of at most one prefill pass's rows each.
-        cfg = self.ctx.cfg
-        cap = max(min(cfg.max_prefill or cfg.max_context, cfg.max_context), cfg.max_streams)
-        group: List[int] = []
-        for k, i in enumerate(live):
-            group.append(i)
-            rows = sum(len(prompts[j]) for j in group)
-            nxt_rows = len(prompts[live[k + 1]]) if k + 1 < len(live) else None
-            if nxt_rows is None or rows + nxt_rows > cap:
-                firsts = self.ctx.prefill_batch([streams[j] for j in group], [prompts[j] for j in group])
-                now = time.perf_counter() - t0
-                for j, f in zip(group, firsts):
-                    out[j].t_first = now
-                    out[j].tokens.append(int(f))
-                group = []
+        # One call for all prompts; the library runs as many passes as the
+        # rows need (a prompt longer than a pass continues in the next one).
+        if live:
+            firsts = self.ctx.prefill_batch([streams[i] for i in live], [prompts[i] for i in live])
+            now = time.perf_counter() - t0
+            for i, f in zip(live, firsts):
+                out[i].t_first = now
+                out[i].tokens.append(_token(int(f)))
         n = len(live)
         if n == 0 or n_tokens == 1:
             for i in live:
@@ -206,6 +208,6 @@ class Server:
             now = time.perf_counter() - t0
             row = self.host[k, :n].tolist()
             for j, i in enumerate(live):
-                out[i].tokens.append(int(row[j]))
+                out[i].tokens.append(_token(int(row[j])))
                 out[i].t_last = now
         return out

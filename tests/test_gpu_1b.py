@@ -130,25 +130,87 @@ def test_multistream_lockstep(one_b, ctx):
     print(f"1B 4-stream decode: max-abs {worst:.4g}")
 
 
-def test_prefill_batch_1b(one_b, ctx):
-    """Three ragged prompts in one hh_prefill_batch pass on the 1B bf16 model
-    (MFMA GEMMs over the packed rows, per-row attention, n-row head): next
-    tokens and the KV each stream is left with, checked by a lockstep decode
-    step, against the oracle's run of each stream alone."""
+@pytest.fixture(scope="module")
+def forced_256(one_b):
+    """The bench prompt (256 tokens, seed 2) and 8 teacher-forced steps of the
+    oracle: (prompt, fed tokens, reference logits of the prompt's last row
+    and of each step)."""
     shape, _, model = one_b
+    prompt = synth.make_tokens(shape.vocab, 256, 2)
+    ref, cache = model.prefill(prompt, rows="last")
+    rows, fed = [ref[0]], []
+    for _ in range(8):
+        fed.append(int(np.argmax(rows[-1])))
+        rows.append(model.decode(cache, fed[-1]))
+    return prompt, fed, rows
+
+
+def forced_run(ctx, forced, what):
+    prompt, fed, rows = forced
+    ctx.reset()
+    _, last = ctx.prefill(0, prompt, logits="last")
+    worst = check_logits(last, rows[0], TOL, what=f"{what} prompt last row")
+    for i, tok in enumerate(fed):
+        _, lg = ctx.decode_step([0], [tok], logits=True)
+        worst = max(worst, check_logits(lg[0], rows[i + 1], TOL, what=f"{what} step {i}"))
+    return worst
+
+
+def test_gemv_graph_path(one_b, forced_256):
+    """The batch-1 path of separate GEMV / attention kernels replayed as a
+    graph (taken when the single-kernel step is switched off, and the side
+    the long-context consistency checks compare with) against the oracle."""
+    shape, tensors, _ = one_b
+    os.environ["HH_STEP_KERNEL"] = "0"
+    try:
+        c = new_context(shape, tensors, streams=1, context=512, max_prefill=256)
+    finally:
+        del os.environ["HH_STEP_KERNEL"]
+    try:
+        worst = forced_run(c, forced_256, "GEMV graph path")
+    finally:
+        c.close()
+    print(f"1B GEMV graph path, 256 prompt + 8 steps: max-abs {worst:.4g}")
+
+
+def test_window_131072_short_use(one_b, forced_256):
+    """The paper's window sweep as stated (a large allocated context, short
+    use): a 131072-position context serving the bench request's prompt and
+    8 decode steps."""
+    shape, tensors, _ = one_b
+    c = new_context(shape, tensors, streams=1, context=131072, max_prefill=256)
+    try:
+        worst = forced_run(c, forced_256, "131072-position window")
+    finally:
+        c.close()
+    print(f"1B in a 131072-position window, 256 prompt + 8 steps: max-abs {worst:.4g}")
+
+
+def test_prefill_batch_1b(one_b, ctx, forced_256):
+    """Ragged prompts in one hh_prefill_batch call on the 1B bf16 model (MFMA
+    GEMMs over the packed rows, per-row attention, n-row head): the bench
+    prompt of 256 tokens (16 pages per row) plus 5 and 40 tokens, 301 rows in
+    two 256-row passes.  Next tokens and the KV each stream is left with,
+    checked by a lockstep decode step, against the oracle's run of each
+    stream alone."""
+    shape, _, model = one_b
+    prompt, fed, rows = forced_256
     ctx.reset()
     ids = [4, 1, 2]
-    prompts = [synth.make_tokens(shape.vocab, n, 400 + n) for n in (77, 5, 40)]
+    prompts = [prompt] + [synth.make_tokens(shape.vocab, n, 400 + n) for n in (5, 40)]
     nxt = ctx.prefill_batch(ids, prompts)
-    caches, worst = [], 0.0
-    for k, p in enumerate(prompts):
+    refs, caches, worst = [rows[0]], [None], 0.0
+    for p in prompts[1:]:
         logits, cache = model.prefill(p, rows="last")
+        refs.append(logits[0])
         caches.append(cache)
-        if top2_margin(logits[0]) > 1e-2:
-            assert int(nxt[k]) == int(np.argmax(logits[0])), f"stream {ids[k]}"
-    feed = np.array([101, 202, 303], dtype=np.int32)
-    _, lg = ctx.decode_step(ids, feed, logits=True)
     for k in range(3):
+        if top2_margin(refs[k]) > 1e-2:
+            assert int(nxt[k]) == int(np.argmax(refs[k])), f"stream {ids[k]}"
+    feed = np.array([fed[0], 202, 303], dtype=np.int32)
+    _, lg = ctx.decode_step(ids, feed, logits=True)
+    worst = check_logits(lg[0], rows[1], TOL, what="1B batch prefill stream 4")
+    for k in (1, 2):
         worst = max(worst, check_logits(lg[k], model.decode(caches[k], int(feed[k])), TOL,
                                         what=f"1B batch prefill stream {ids[k]}"))
-    print(f"1B batch prefill (77, 5, 40 rows) then lockstep step: max-abs {worst:.4g}")
+    print(f"1B batch prefill (256, 5, 40 rows) then lockstep step: max-abs {worst:.4g}")

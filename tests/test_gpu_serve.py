@@ -91,3 +91,27 @@ def test_batch_of_requests_in_lockstep(tiny_server):
         assert 0 < a.t_first <= a.t_last
     with pytest.raises(ValueError):
         srv.answer_batch(queries[:2], 4, streams=[0])
+
+
+def test_batch_prompts_longer_than_a_pass(tiny_server):
+    """Rendered prompts longer than one prefill pass (max_prefill 32 rows):
+    the batch prefill continues each prompt in the next pass, and every
+    stream still decodes the oracle's greedy continuation."""
+    shape, model, store, _, _ = tiny_server
+    tensors = synth.make_weights(shape, 0, gain_std=0.1)
+    ctx = new_context(shape, tensors, streams=4, context=256, max_prefill=32)
+    router = serve.Router([t for t, _ in store])
+    try:
+        srv = serve.Server(ctx, router, [a for _, a in store], max_tokens=12, max_batch=3)
+        texts = [t for t, _ in store]
+        queries = [q for q, _ in synth.make_queries(store, 2, seed=24) if not orc.route(texts, q)[2]][:3]
+        answers = srv.answer_batch(queries, 12, streams=[2, 0, 3])
+        for s, (q, a) in zip([2, 0, 3], zip(queries, answers)):
+            prompt = serve.byte_tokens(orc.render_marker(store[a.entry][1]).encode())
+            assert len(prompt) > 32
+            assert len(a.tokens) == 12
+            assert list(ctx.read_argmax(s, len(prompt) - 1, 12)) == a.tokens
+            check_greedy(model, prompt, a.tokens, q)
+    finally:
+        router.close()
+        ctx.close()

@@ -126,15 +126,16 @@ def test_prefill_between_lockstep_steps(tiny):
 
 
 def test_prefill_batch_matches_oracle(tiny):
-    """Several streams' prompts in one pass (ragged, one of a single token,
-    one appended to a stream that already holds tokens): each stream's next
-    token and the KV it leaves (checked by a lockstep decode step) equal the
-    oracle's run of that stream alone."""
+    """Several streams' prompts in one call (ragged, one of a single token,
+    one appended to a stream that already holds tokens, one of 230 tokens
+    whose rows attend over 15 pages; 331 rows, so the 256-row passes split
+    the last prompt): each stream's next token and the KV it leaves (checked
+    by a lockstep decode step) equal the oracle's run of that stream alone."""
     shape, tensors, model = tiny
     ctx = new_context(shape, tensors, streams=6)
     head = synth.make_tokens(shape.vocab, 10, 310)
     ctx.prefill(2, head)
-    lens = {0: 1, 2: 7, 3: 30, 5: 64}
+    lens = {0: 1, 2: 7, 3: 93, 5: 230}
     prompts = {s: synth.make_tokens(shape.vocab, n, 320 + s) for s, n in lens.items()}
     ids = [3, 0, 5, 2]
     nxt = ctx.prefill_batch(ids, [prompts[s] for s in ids])
@@ -152,7 +153,7 @@ def test_prefill_batch_matches_oracle(tiny):
     for k, s in enumerate(ids):
         check_logits(lg[k], model.decode(caches[s], int(feed[k])), TOL, what=f"after batch prefill, stream {s}")
     from paper_2606_12154_amd import hh
-    for bad_ids, bad_prompts in [([1, 1], [[5], [6]]), ([1], [[]]), ([1, 4], [[1] * 200, [2] * 100])]:
+    for bad_ids, bad_prompts in [([1, 1], [[5], [6]]), ([1], [[]]), ([1, 4], [[1] * 3, [4096]])]:
         with pytest.raises(hh.HHError) as e:
             ctx.prefill_batch(bad_ids, bad_prompts)
         assert e.value.status == hh.HH_ERR_INVALID_ARG
@@ -241,5 +242,74 @@ def test_stale_arena_contents(tiny):
         check_logits(lg, model.decode_batch(caches, feed), TOL, what="multi decode")
         _, lg = ctx.decode_step([2], [11], logits=True)  # batch-1 kernel on the 1-token stream
         check_logits(lg[0], model.decode(caches[2], 11), TOL, what="single decode")
+    finally:
+        ctx.close()
+
+
+@pytest.mark.parametrize("var,value", [("HH_RING_SLOTS", "6"), ("HH_LOAD_DEPTH", "1"), ("HH_LOAD_DEPTH", "7"),
+                                       ("HH_STEP_QUIET", "1"), ("HH_STEP_QUIET", "2"), ("HH_POLL_DELAY", "0"),
+                                       ("HH_POLL_DELAY", "400")])
+def test_step_schedule_variants(tiny, var, value):
+    """The single-kernel decode step's schedule settings (ring slots, loads
+    in flight per streaming wave, pausing the streams during exchange waits,
+    delay before the first poll) change timing only: teacher-forced logits
+    still match the oracle."""
+    import os
+    shape, tensors, model = tiny
+    prompt = synth.make_tokens(shape.vocab, 64, 1)
+    toks, ref = oracle_greedy(model, prompt, 8)
+    os.environ[var] = value
+    try:
+        ctx = new_context(shape, tensors, streams=1, context=96)
+    finally:
+        del os.environ[var]
+    try:
+        ctx.prefill(0, prompt)
+        for i in range(8):
+            _, lg = ctx.decode_step([0], [int(toks[i])], logits=True)
+            check_logits(lg[0], ref[i + 1], TOL, what=f"{var}={value} step {i}")
+    finally:
+        ctx.close()
+
+
+def test_failed_step_is_reported(tiny):
+    """A decode step whose bounded wait gives up (forced from the host: the
+    final argmax wait expects an epoch no workgroup publishes, with a 10 us
+    limit; every wave still runs to its end) leaves -1 as its token, later
+    device-fed steps of the stream and multi-stream steps including it keep
+    -1, the first call with host outputs returns HH_ERR_HIP, and hh_reset
+    brings the stream back."""
+    import os
+    from paper_2606_12154_amd import hh
+    shape, tensors, model = tiny
+    p0 = synth.make_tokens(shape.vocab, 40, 61)
+    p1 = synth.make_tokens(shape.vocab, 24, 62)
+    os.environ["HH_STEP_WAIT_TICKS"] = "1000"
+    os.environ["HH_STEP_FAIL_WAIT"] = "1"
+    try:
+        ctx = new_context(shape, tensors, streams=2, context=96)
+    finally:
+        del os.environ["HH_STEP_WAIT_TICKS"]
+        del os.environ["HH_STEP_FAIL_WAIT"]
+    try:
+        ctx.prefill(0, p0)
+        ctx.prefill(1, p1)
+        for _ in range(3):
+            ctx.decode_step([0], None, host_next=False)
+        assert list(ctx.read_argmax(0, 40, 3)) == [-1, -1, -1]
+        ref1, cache1 = model.prefill(p1, rows="last")
+        ctx.decode_step([0, 1], None, host_next=False)  # the multi-row path
+        assert int(ctx.read_argmax(0, 43, 1)[0]) == -1
+        ref = model.decode(cache1, int(np.argmax(ref1[0])))
+        if top2_margin(ref) > 1e-2:
+            assert int(ctx.read_argmax(1, 24, 1)[0]) == int(np.argmax(ref))
+        with pytest.raises(hh.HHError) as e:
+            ctx.decode_step([0], [5], logits=True)
+        assert e.value.status == hh.HH_ERR_HIP
+        ctx.reset()
+        nxt, last = ctx.prefill(0, p0, logits="last")
+        ref0, _ = model.prefill(p0, rows="last")
+        check_logits(last, ref0[0], TOL, what="prefill after reset")
+        assert nxt == int(np.argmax(ref0[0]))
     finally:
         ctx.close()
