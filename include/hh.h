@@ -175,6 +175,31 @@ hh_status hh_prefill_batch(hh_ctx* ctx, int32_t n, const int32_t* stream_ids, co
 hh_status hh_decode_step(hh_ctx* ctx, int32_t n_streams, const int32_t* stream_ids,
                          const int32_t* tokens, float* logits, int32_t* next_tokens);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): one greedy
+ * batch-1 decode step of stream_id, as hh_decode_step with n_streams == 1,
+ * whose cross-workgroup exchange words live in a fixed array the library
+ * keeps in each device's memory (9 MiB per device, held until the process
+ * ends) instead of the context's arena.  The call allocates nothing and
+ * captures no graph: it enqueues a small fill of the array's error word and
+ * the single-kernel step on the context's stream.
+ *  token        host, one id to consume, or NULL for the stream's pending
+ *               token.
+ *  logits       NULL or [vocab] fp32, host or device.
+ *  next_token   NULL or one int32, host or device.
+ * Every context on a device shares that device's array, and it keeps the
+ * last step's contents: steps of different contexts that overlap in time on
+ * one device (different streams, no ordering between them) race and give
+ * wrong results.  Steps in one stream's order are safe.
+ * Errors: as hh_decode_step; UNSUPPORTED when the configuration has no
+ * single-kernel step or needs more exchange words than the array holds
+ * (d_model 2048 with 32 query heads fits up to 256 workgroups); INVALID_ARG
+ * when the context's device is not the current one.
+ */
+hh_status hh_decode_step_noalloc(hh_ctx* ctx, int32_t stream_id, const int32_t* token, float* logits,
+                                 int32_t* next_token);
+
 /* Drop a stream's KV pages and set its length to 0 (stream_id -1: all).
  * Also clears the context's record of a failed decode step (see
  * hh_decode_step). */

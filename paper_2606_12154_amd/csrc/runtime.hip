@@ -11,6 +11,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <tuple>
 #include <type_traits>
@@ -80,7 +81,7 @@ bool config_supported(const hh_config& c, std::string& why) {
 }
 
 // Where the decode-step kernel's exchange words live: the context's arena
-// (the default), or another buffer of the same layout.
+// (hh_decode_step) or the fixed device array (hh_decode_step_noalloc).
 // Layout for up to `cap` workgroups: xa, xb [d], q [Hq*64], kn, vn
 // [Hkv*64], attention partials [Hq][cap][66], o [Hq*64], down partials
 // [cap][d], argmax keys [2*cap], then the error word.
@@ -224,6 +225,7 @@ struct hh_ctx {
   int step_wg = 0;     // workgroups of the persistent batch-1 decode kernel (0: not usable)
   bool step_q4 = false;  // the persistent kernel streams the stored 4-bit rows
   unsigned step_count = 0;  // persistent-kernel launches so far (names each step's epochs)
+  int device = 0;           // HIP device current at hh_create
   int step_depth = kStepLoadDepth;  // HH_LOAD_DEPTH: ring slots in flight per streaming wave
   int step_quiet = 0;               // HH_STEP_QUIET: pause streaming during exchange waits
   int step_ring = kStepRingSlots;   // HH_RING_SLOTS: LDS ring slots used (at most kStepRingSlots)
@@ -756,6 +758,45 @@ hh_status finish(hh_ctx* c, bool host_out, const int* err_word = nullptr) {
   return HH_OK;
 }
 
+// ---------------------------------------------------------------- allocation-free decode step
+
+// Exchange words of hh_decode_step_noalloc: a fixed array in every device's
+// memory (each GPU the library runs on holds its own copy until the process
+// ends).  In host code `scratch` names a host-side stand-in, not device
+// memory: only the address hipGetSymbolAddress returns for the current
+// device is ever passed to kernels or copies.
+constexpr size_t kScratchWords = (size_t)9 << 17;  // 9 MiB of 8-byte words
+static __device__ __align__(256) unsigned long long scratch[kScratchWords];
+
+constexpr int kMaxDevices = 64;
+struct ScratchTable {
+  std::mutex mu;
+  unsigned long long* ptr[kMaxDevices] = {};
+  hipError_t rc[kMaxDevices] = {};
+  unsigned steps[kMaxDevices] = {};  // noalloc steps launched on the device (names their epochs)
+};
+ScratchTable& scratch_table() {
+  static ScratchTable t;
+  return t;
+}
+
+// Once per device, with that device current: the device address of its copy.
+void scratch_setup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return;
+  ScratchTable& t = scratch_table();
+  std::lock_guard<std::mutex> lk(t.mu);
+  if (t.ptr[dev] || t.rc[dev] != hipSuccess) return;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e == hipSuccess && p) t.ptr[dev] = static_cast<unsigned long long*>(p);
+  else t.rc[dev] = e != hipSuccess ? e : hipErrorInvalidSymbol;
+}
+
+__global__ void k_zero_words(unsigned long long* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0ull;
+}
+
 }  // namespace
 
 extern "C" {
@@ -779,6 +820,8 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   c->L = L;
   c->arena = static_cast<char*>(arena);
   c->stream = static_cast<hipStream_t>(hip_stream);
+  if (hipGetDevice(&c->device) != hipSuccess) c->device = -1;
+  scratch_setup(c->device);
   const char* tp = std::getenv("HH_STEP_TRACE");
   if (tp) c->trace_path = tp;
   if (const char* q = std::getenv("HH_STEP_QUIET")) c->step_quiet = std::atoi(q);
@@ -1007,6 +1050,52 @@ hh_status hh_decode_step(hh_ctx* c, int32_t n, const int32_t* stream_ids, const 
                                     : do_decode<float, float, float>(c, n, ids, tokens, logits, next);
   if (rc != HH_OK) return rc;
   return finish(c, (logits && !is_device_ptr(logits)) || (next && !is_device_ptr(next)));
+}
+
+hh_status hh_decode_step_noalloc(hh_ctx* c, int32_t s, const int32_t* token, float* logits, int32_t* next) {
+  if (!c) return HH_ERR_INVALID_ARG;
+  if (!c->loaded) return c->fail(HH_ERR_NOT_LOADED, "weights not loaded");
+  const hh_config& g = c->cfg;
+  if (s < 0 || s >= g.max_streams) return c->fail(HH_ERR_INVALID_ARG, "stream id out of range");
+  if (c->step_wg <= 0)
+    return c->fail(HH_ERR_UNSUPPORTED, "the single-kernel decode step is not available for this configuration");
+  const size_t need = step_words(g, (size_t)c->step_wg);
+  if (need > kScratchWords)
+    return c->fail(HH_ERR_UNSUPPORTED, "exchange words exceed the fixed array (" + std::to_string(need) + " > " +
+                                           std::to_string(kScratchWords) + " words)");
+  if (c->device < 0 || c->device >= kMaxDevices) return c->fail(HH_ERR_HIP, "no HIP device recorded for the context");
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != c->device)
+    return c->fail(HH_ERR_INVALID_ARG, "the context's device is not the current device");
+  if (c->len[s] + 1 > g.max_context) return c->fail(HH_ERR_CONTEXT_FULL, "stream at max_context");
+  if (!token && c->len[s] == 0) return c->fail(HH_ERR_INVALID_ARG, "empty stream needs an explicit token");
+  if (token && (*token < 0 || *token >= g.vocab)) return c->fail(HH_ERR_INVALID_ARG, "token id out of range");
+  const int have = (int)c->pages[s].size();
+  if ((c->len[s] + 1 + kPage - 1) / kPage > have && c->free_pages.empty())
+    return c->fail(HH_ERR_CONTEXT_FULL, "KV page pool exhausted");
+  ScratchTable& t = scratch_table();
+  StepWords w{nullptr, (size_t)c->step_wg, 0};
+  {
+    std::lock_guard<std::mutex> lk(t.mu);
+    if (!t.ptr[c->device]) {
+      c->err = std::string("fixed exchange array: hipGetSymbolAddress: ") + hipGetErrorString(t.rc[c->device]);
+      return HH_ERR_HIP;
+    }
+    w.base = t.ptr[c->device];
+    // Epochs are counted per device, across contexts, so the words another
+    // context left in the array never look current to this step.
+    t.steps[c->device] += 1;
+    w.epoch = t.steps[c->device] * 512u;
+  }
+  // The error word must start at zero (a fill kernel: capture-safe).
+  const int n_err = 8;
+  k_zero_words<<<1, 64, 0, c->stream>>>(w.base + need - n_err, n_err);
+  HIPCHK(c, hipGetLastError());
+  const std::vector<int> ids{s};
+  hh_status rc = g.dtype == HH_BF16 ? do_decode<__bf16, _Float16, _Float16>(c, 1, ids, token, logits, next, &w)
+                                    : do_decode<float, float, float>(c, 1, ids, token, logits, next, &w);
+  if (rc != HH_OK) return rc;
+  return finish(c, (logits && !is_device_ptr(logits)) || (next && !is_device_ptr(next)), step_err_word(g, w));
 }
 
 hh_status hh_reset(hh_ctx* c, int32_t s) {

@@ -24,7 +24,7 @@ HH_LOGITS_NONE, HH_LOGITS_LAST, HH_LOGITS_ALL = 0, 1, 2
 HH_WF_DTYPE, HH_WF_Q4G32 = 0, 1
 
 EXPORTED = ["hh_workspace_size", "hh_create", "hh_load_weights", "hh_prefill", "hh_prefill_batch", "hh_decode_step",
-            "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error",
+            "hh_decode_step_noalloc", "hh_reset", "hh_stream_length", "hh_read_argmax", "hh_destroy", "hh_last_error",
             "hh_q4g32_quantize", "hh_router_create", "hh_router_query", "hh_router_route",
             "hh_router_size", "hh_router_destroy", "hh_render_marker", "hh_read_probe"]
 
@@ -63,6 +63,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "hh_prefill": ([c_void_p, c_int32, i32p, c_int32, c_int32, c_void_p, c_void_p], c_int32),
         "hh_decode_step": ([c_void_p, c_int32, i32p, i32p, c_void_p, c_void_p], c_int32),
         "hh_prefill_batch": ([c_void_p, c_int32, i32p, i32p, i32p, c_void_p], c_int32),
+        "hh_decode_step_noalloc": ([c_void_p, c_int32, i32p, c_void_p, c_void_p], c_int32),
         "hh_reset": ([c_void_p, c_int32], c_int32),
         "hh_stream_length": ([c_void_p, c_int32, i32p], c_int32),
         "hh_read_argmax": ([c_void_p, c_int32, c_int32, c_int32, i32p], c_int32),
@@ -127,6 +128,12 @@ def hh_decode_step(ctx: int, n_streams: int, stream_ids, tokens, logits_ptr, nex
     _check(ctx, load_library().hh_decode_step(
         ctx, n_streams, None if ids is None else ids.ctypes.data_as(POINTER(c_int32)),
         None if tok is None else tok.ctypes.data_as(POINTER(c_int32)), logits_ptr, next_ptr))
+
+
+def hh_decode_step_noalloc(ctx: int, stream_id: int, token, logits_ptr, next_ptr) -> None:
+    tok = None if token is None else np.array([token], dtype=np.int32)
+    _check(ctx, load_library().hh_decode_step_noalloc(
+        ctx, stream_id, None if tok is None else tok.ctypes.data_as(POINTER(c_int32)), logits_ptr, next_ptr))
 
 
 def hh_reset(ctx: int, stream_id: int) -> None:
