@@ -33,6 +33,10 @@ struct DecodeKernels {
 void finalize(hipStream_t st, int r0, int n, const int* row_stream, const int* row_pos, unsigned long long* slot,
               int* pending, int* hist, int* pos, int max_ctx);
 
+// dst[0 .. n) = src[0 .. n) (host ints) through kernel arguments, kPutInts per launch.
+constexpr int kPutInts = 62;
+void put_ints(hipStream_t st, int* dst, const int* src, int n);
+
 // fp32 scratch (in the context's arena) for split-K partial tiles of the
 // MFMA GEMM; splits are reduced until the partials fit.
 struct GemmWorkspace {

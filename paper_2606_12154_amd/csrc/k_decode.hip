@@ -692,6 +692,25 @@ void DecodeKernels<TW, TKV, TM>::rmsnorm_rows(hipStream_t st, int n_rows, const 
   k_rmsnorm_rows<TM><<<n_rows, 256, 0, st>>>(x, gain, eps, d, h);
 }
 
+// Small host integer arrays (page ids, stream lists, teacher-forced tokens)
+// reach the device as kernel arguments, not as copies from pageable memory.
+struct IntArgs {
+  int n;
+  int v[kPutInts];
+};
+__global__ void k_put_ints(int* __restrict__ dst, IntArgs a) {
+  if ((int)threadIdx.x < a.n) dst[threadIdx.x] = a.v[threadIdx.x];
+}
+
+void put_ints(hipStream_t st, int* dst, const int* src, int n) {
+  for (int o = 0; o < n; o += kPutInts) {
+    IntArgs a;
+    a.n = n - o < kPutInts ? n - o : kPutInts;
+    for (int i = 0; i < a.n; ++i) a.v[i] = src[o + i];
+    k_put_ints<<<1, 64, 0, st>>>(dst + o, a);
+  }
+}
+
 void finalize(hipStream_t st, int r0, int n, const int* row_stream, const int* row_pos, unsigned long long* slot,
               int* pending, int* hist, int* pos, int max_ctx) {
   k_finalize<<<1, 64, 0, st>>>(r0, n, row_stream, row_pos, slot, pending, hist, pos, max_ctx);

@@ -542,10 +542,14 @@ __global__ __launch_bounds__(256) void k_splitk_finalize(const float* __restrict
 // epilogue runs from the accumulators: column pairs (c, c + 32) of a 64-column
 // group sit in one lane (blocks 2g and 2g + 1 of the wave), which is the pairing
 // every register epilogue needs (rotary halves, gate / up).
-template <int BM, int BN>
+template <int BM, int BN, int NW_ = 4>
 struct WideTile {
-  static constexpr int BK = 64, NW = 4, THREADS = 256;
-  static constexpr int WM = BM / 2, WN = BN / 2;     // wave block
+  static constexpr int BK = 64, NW = NW_, THREADS = 64 * NW_;
+  // Wave grid: 2 x 2 with four waves; with eight (two per SIMD, so one
+  // wave's MFMAs run while the other waits on LDS or a barrier) 2 x 4 for
+  // 256-wide tiles, else 4 x 2, so a wave block keeps whole 64-column groups.
+  static constexpr int WGM = NW == 4 ? 2 : (BN >= 256 ? 2 : 4), WGN = NW / WGM;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave block
   static constexpr int FM = WM / 32, FN = WN / 32;   // 32x32 MFMA blocks per wave
   static constexpr int GROUPS = (BM + BN) / 8;       // 1 KiB row groups per stage
   static constexpr int NI = GROUPS / NW;             // load instructions per wave per stage
@@ -558,23 +562,23 @@ struct WideTile {
   static_assert((NSTAGE - 1) * NI <= 63, "in-flight loads fit the vmcnt range");
 };
 
-template <int BM, int BN, class Epi>
-__global__ __launch_bounds__(256, 1) void k_gemm_wide(const _Float16* __restrict__ A, int M,
-                                                      const _Float16* __restrict__ W, int K, int ntn, int ntiles,
-                                                      int steps_per_split, float* __restrict__ partial, int ncols,
-                                                      Epi epi) {
-  using T = WideTile<BM, BN>;
+template <int BM, int BN, int NW, class Epi>
+__global__ __launch_bounds__(64 * NW, 1) void k_gemm_wide(const _Float16* __restrict__ A, int M,
+                                                          const _Float16* __restrict__ W, int K, int ntn, int ntiles,
+                                                          int steps_per_split, float* __restrict__ partial, int ncols,
+                                                          Epi epi) {
+  using T = WideTile<BM, BN, NW>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tile = blockIdx.x % ntiles, split = blockIdx.x / ntiles;
   const int tn = tile % ntn, tm = tile / ntn;
   const int m0 = tm * BM, n0 = tn * BN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
   const int nk_all = K / T::BK;
   const int s0 = split * steps_per_split;
   const int nk = min(nk_all, s0 + steps_per_split) - s0;
 
-  // Instruction q of wave w fills row group g = w + 4q (stage rows 8g .. 8g + 7):
+  // Instruction q of wave w fills row group g = w + NW q (stage rows 8g .. 8g + 7):
   // lane l takes row 8g + l/8, k chunk (l%8) ^ swz(row), swz(r) = (r/2) % 8.
   const _Float16* src[T::NI];
 #pragma unroll
@@ -725,13 +729,13 @@ static int launch_f16(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M
   return splits;
 }
 
-template <int BM, int BN, class Epi>
+template <int BM, int BN, int NW = 4, class Epi>
 static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* W, int K, int n_cols,
                        int splits, const Epi& e, bool defer) {
-  using T = WideTile<BM, BN>;
+  using T = WideTile<BM, BN, NW>;
   static bool attr = false;
   if (!attr) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_wide<BM, BN, Epi>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_wide<BM, BN, NW, Epi>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS);
     attr = true;
   }
@@ -743,7 +747,8 @@ static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
   const int per = (nk + splits - 1) / splits;
   splits = (nk + per - 1) / per;
   float* part = splits > 1 ? ws.ptr : nullptr;
-  k_gemm_wide<BM, BN, Epi><<<ntiles * splits, T::THREADS, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols, e);
+  k_gemm_wide<BM, BN, NW, Epi><<<ntiles * splits, T::THREADS, T::LDS, st>>>(A, M, W, K, ntn, ntiles, per, part, n_cols,
+                                                                            e);
   if (splits > 1 && !defer)
     k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ntn * (BN / 128), 256, 0, st>>>(part, splits, M, n_cols,
                                                                                              ntn * (BN / 128), e);
@@ -920,7 +925,7 @@ static int launch_skinny(hipStream_t st, GemmWorkspace ws, const _Float16* A, in
 // small-tile kernel.  HH_GEMM_QKV / _RESID (O projection) / _DOWN / _GATEUP =
 // "BMxBNxS" (or "0") overrides it, for tuning.
 struct WideCfg {
-  int bm, bn, splits;
+  int bm, bn, splits, nw;  // nw: waves per workgroup (4 or 8)
 };
 
 static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
@@ -928,9 +933,9 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
   // The down projection (K > N) has a knob of its own.
   const char* env = getenv(kind == GemmKind::Resid && K > n_cols ? "HH_GEMM_DOWN" : names[(int)kind]);
   if (env) {
-    WideCfg c{0, 0, 1};
-    if (sscanf(env, "%dx%dx%d", &c.bm, &c.bn, &c.splits) >= 2) return c;
-    return WideCfg{0, 0, 1};
+    WideCfg c{0, 0, 1, 4};
+    if (sscanf(env, "%dx%dx%dx%d", &c.bm, &c.bn, &c.splits, &c.nw) >= 2) return c;
+    return WideCfg{0, 0, 1, 4};
   }
   // Measured on the 1B prompt shapes (d 2048, FFN 8192): gate/up at 1024 rows
   // takes 256 x 128 tiles (512 tiles, two rounds of the CUs; TTFT 3.74 ->
@@ -939,11 +944,13 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
   // everything at 256 rows, stay on the small-tile kernel, whose two
   // workgroups per CU suit these few-tile shapes better.
   if (kind == GemmKind::GateUp && n_cols >= 8192) {
-    if (M >= 512) return WideCfg{256, 128, 1};
-    if (M >= 256) return WideCfg{128, 128, 1};
+    // Eight waves (two per SIMD) here: TTFT at 1024 rows 3.66 -> 3.57 ms;
+    // every other shape was slower with eight.
+    if (M >= 512) return WideCfg{256, 128, 1, 8};
+    if (M >= 256) return WideCfg{128, 128, 1, 4};
   }
-  if (kind == GemmKind::Resid && M >= 512) return WideCfg{128, 128, 2};
-  return WideCfg{0, 0, 1};
+  if (kind == GemmKind::Resid && M >= 512) return WideCfg{128, 128, 2, 4};
+  return WideCfg{0, 0, 1, 4};
 }
 
 // Returns the splits used, 0 when the shape is left to the small-tile kernel.
@@ -952,6 +959,12 @@ static int run_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, 
                     const Epi& e, GemmKind kind, bool defer) {
   if (kind == GemmKind::Logits || M < 128) return 0;
   const WideCfg c = wide_choice(kind, M, n_cols, K);
+  if (c.nw == 8) {
+    if (c.bm == 256 && c.bn == 256) return launch_wide<256, 256, 8>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+    if (c.bm == 256 && c.bn == 128) return launch_wide<256, 128, 8>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+    if (c.bm == 128 && c.bn == 256) return launch_wide<128, 256, 8>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
+    return 0;
+  }
   if (c.bm == 256 && c.bn == 256) return launch_wide<256, 256>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
   if (c.bm == 256 && c.bn == 128) return launch_wide<256, 128>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);
   if (c.bm == 128 && c.bn == 256) return launch_wide<128, 256>(st, ws, A, M, W, K, n_cols, c.splits, e, defer);

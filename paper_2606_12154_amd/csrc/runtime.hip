@@ -504,8 +504,8 @@ hh_status ensure_pages(hh_ctx* c, int s, int new_len) {
     c->free_pages.pop_back();
   }
   int* dst = c->at<int>(c->L.page_table) + (size_t)s * c->L.max_pages + first_new;
-  HIPCHK(c, hipMemcpyAsync(dst, pg.data() + first_new, (need - first_new) * sizeof(int), hipMemcpyHostToDevice,
-                           c->stream));
+  put_ints(c->stream, dst, pg.data() + first_new, need - first_new);
+  HIPCHK(c, hipGetLastError());
   return HH_OK;
 }
 
@@ -673,10 +673,14 @@ hh_status do_decode(hh_ctx* c, int n, const std::vector<int>& ids, const int32_t
     if (rc != HH_OK) return rc;
   }
   if (c->uploaded_streams != ids) {
-    HIPCHK(c, hipMemcpyAsync(c->at<int>(L.row_stream), ids.data(), n * sizeof(int), hipMemcpyHostToDevice, st));
+    put_ints(st, c->at<int>(L.row_stream), ids.data(), n);
+    HIPCHK(c, hipGetLastError());
     c->uploaded_streams = ids;
   }
-  if (tokens) HIPCHK(c, hipMemcpyAsync(c->at<int>(L.feed), tokens, n * sizeof(int), hipMemcpyHostToDevice, st));
+  if (tokens) {
+    put_ints(st, c->at<int>(L.feed), tokens, n);
+    HIPCHK(c, hipGetLastError());
+  }
   const bool want_logits = logits != nullptr;
   if (n == 1 && (c->step_wg > 0 || words)) {
     // Each step owns 512 epochs (8 phases x 64 layers); epoch 0 is never

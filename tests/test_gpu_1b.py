@@ -69,11 +69,13 @@ def test_prefill_appended_chunk(one_b, ctx, prompt_ref, cut):
 GEMM_KINDS = ("HH_GEMM_QKV", "HH_GEMM_RESID", "HH_GEMM_DOWN", "HH_GEMM_GATEUP")
 
 
-@pytest.mark.parametrize("tile", ["256x256x1", "256x128x1", "128x256x1", "128x128x1", "256x256x4", "128x128x2"])
+@pytest.mark.parametrize("tile", ["256x256x1", "256x128x1", "128x256x1", "128x128x1", "256x256x4", "128x128x2",
+                                  "256x256x1x8", "256x128x2x8", "128x256x1x8"])
 @pytest.mark.parametrize("n", [256, 200])
 def test_prefill_wide_tiles(one_b, ctx, prompt_ref, tile, n):
-    """Every large-tile GEMM shape (and split-K) of the prompt path, forced
-    for the QKV, residual and gate/up GEMMs, on a whole and a ragged row count."""
+    """Every large-tile GEMM shape (and split-K; four or eight waves per
+    workgroup) of the prompt path, forced for the QKV, residual and gate/up
+    GEMMs, on a whole and a ragged row count."""
     toks, ref = prompt_ref
     saved = {k: os.environ.get(k) for k in GEMM_KINDS}
     try:
