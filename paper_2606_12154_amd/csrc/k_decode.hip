@@ -458,8 +458,8 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ p
 // Paged GQA attention for decode rows: one 512-thread workgroup per (row,
 // kv head) serves the G query heads of that kv head, so each K/V page is
 // read once.  The row's page list is staged in LDS; wave w takes pages w,
-// w + 8, ... with the next page's K/V in flight in a second register set
-// (strict alternation, no register copies).  Lane (key = lane / 4, quarter =
+// w + 8, ... with the next two pages' K/V in flight in two more register
+// sets (strict rotation, no register copies).  Lane (key = lane / 4, quarter =
 // lane % 4) holds 16 dims of one key; scores use exp2 with 1/sqrt(64)*log2(e)
 // folded into q; each head keeps its own online softmax state.  The waves'
 // states are merged in LDS, one wave per head.
@@ -545,16 +545,22 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       m[h] = mn;
     }
   };
-  // Pages wave, wave + 8, ...; loads past the end re-read the row's last page.
+  // Pages wave, wave + 8, ...: the next two pages' K/V are in flight while
+  // one is taken (three register sets in rotation); loads past the end
+  // re-read the row's last page.
   if (wave < npg) {
-    KvPage<TKV> A, B;
+    KvPage<TKV> A, B, C;
     kv_page_load(A, kv, L, layer, page_of(wave), g, key, quarter);
-    for (int pg = wave; pg < npg; pg += 2 * NW) {
-      kv_page_load(B, kv, L, layer, page_of(min(pg + NW, npg - 1)), g, key, quarter);
+    kv_page_load(B, kv, L, layer, page_of(min(wave + NW, npg - 1)), g, key, quarter);
+    for (int pg = wave; pg < npg; pg += 3 * NW) {
+      kv_page_load(C, kv, L, layer, page_of(min(pg + 2 * NW, npg - 1)), g, key, quarter);
       take(A, pg);
       if (pg + NW >= npg) break;
-      kv_page_load(A, kv, L, layer, page_of(min(pg + 2 * NW, npg - 1)), g, key, quarter);
+      kv_page_load(A, kv, L, layer, page_of(min(pg + 3 * NW, npg - 1)), g, key, quarter);
       take(B, pg + NW);
+      if (pg + 2 * NW >= npg) break;
+      kv_page_load(B, kv, L, layer, page_of(min(pg + 4 * NW, npg - 1)), g, key, quarter);
+      take(C, pg + 2 * NW);
     }
   }
   // Per head: reduce over the keys of each row of 16 lanes (lanes sharing

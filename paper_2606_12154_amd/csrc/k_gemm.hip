@@ -46,11 +46,18 @@ struct EpiQKV {
   __device__ int b_row(int n) const { return n < (hq + 2 * hkv) * 64 ? n : -1; }
   // Rotary pair (i, i + 32) of head `head` in row `row`, unscaled.
   __device__ void head_pair(int row, int head, int i, float y0, float y1) const {
+    const int p = row_pos[row];
+    head_pair_at(row, head, i, y0, y1, p, page_table[(size_t)row_stream[row] * L.max_pages + p / kPage]);
+  }
+  // The same with the row's position p and the KV page holding it given.
+  __device__ void head_pair_at(int row, int head, int i, float y0, float y1, int p, int page) const {
+    head_pair_cs(row, head, i, y0, y1, p, page, head < hq + hkv ? rope[(size_t)p * 32 + i] : make_float2(1.f, 0.f));
+  }
+  // ... and with the rotation's (cos, sin) at (p, i) given.
+  __device__ void head_pair_cs(int row, int head, int i, float y0, float y1, int p, int page, float2 cs) const {
     y0 *= scale;
     y1 *= scale;
-    const int s = row_stream[row], p = row_pos[row];
     if (head < hq + hkv) {
-      const float2 cs = rope[(size_t)p * 32 + i];
       const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
       if (head < hq) {
         if (q) {
@@ -62,13 +69,11 @@ struct EpiQKV {
           qM[((size_t)row * hq + head) * 64 + i + 32] = (TKV)r1;
         }
       } else {
-        const int page = page_table[(size_t)s * L.max_pages + p / kPage];
         TKV* dst = kv + L.head_tile(layer, page, 0, head - hq) + (p % kPage) * 64;
         dst[i] = (TKV)r0;
         dst[i + 32] = (TKV)r1;
       }
     } else {
-      const int page = page_table[(size_t)s * L.max_pages + p / kPage];
       TKV* dst = kv + L.head_tile(layer, page, 1, head - hq - hkv) + (p % kPage) * 64;
       dst[i] = (TKV)y0;
       dst[i + 32] = (TKV)y1;
@@ -81,59 +86,93 @@ struct EpiQKV {
   }
   // A wave's whole in-range 64-column group (one head) for FM x 16 rows:
   // element e of accumulator block i is row rb + 32 i + 8 (e / 4) + e % 4.
-  // The head's kind is decided once for all its rows.
+  // The head's kind is decided once for all its rows.  Per block of 16 rows,
+  // every lookup (positions, rotations, KV pages) is loaded before any
+  // store: the stores may alias the tables as far as the compiler can tell,
+  // so interleaved they would serialise one round trip per element.
   template <int FM>
   __device__ void group_full(int rb, int cb, int c, const f32x16* a0, const f32x16* a1) const {
     const int head = cb / 64;
-    if (head < hq) {
+    const bool isq = head < hq, isk = !isq && head < hq + hkv;
+    const int kvh = isq ? 0 : isk ? head - hq : head - hq - hkv;
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i) {
+      int p[16], sr[16], pg[16];
+      float2 cs[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = rb + 32 * i + 8 * (e >> 2) + (e & 3);
-          const float y0 = a0[i][e] * scale, y1 = a1[i][e] * scale;
-          const float2 cs = rope[(size_t)row_pos[row] * 32 + c];
-          const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+      for (int e = 0; e < 16; ++e) {
+        const int row = rb + 32 * i + 8 * (e >> 2) + (e & 3);
+        p[e] = row_pos[row];
+        if (!isq) sr[e] = row_stream[row];
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        cs[e] = isq || isk ? rope[(size_t)p[e] * 32 + c] : make_float2(1.f, 0.f);
+        if (!isq) pg[e] = page_table[(size_t)sr[e] * L.max_pages + p[e] / kPage];
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = rb + 32 * i + 8 * (e >> 2) + (e & 3);
+        float y0 = a0[i][e] * scale, y1 = a1[i][e] * scale;
+        if (isq || isk) {
+          const float r0 = y0 * cs[e].x - y1 * cs[e].y, r1 = y1 * cs[e].x + y0 * cs[e].y;
+          y0 = r0;
+          y1 = r1;
+        }
+        if (isq) {
           const size_t o = ((size_t)row * hq + head) * 64 + c;
           if (q) {
-            q[o] = r0;
-            q[o + 32] = r1;
+            q[o] = y0;
+            q[o + 32] = y1;
           }
           if (qM) {
-            qM[o] = (TKV)r0;
-            qM[o + 32] = (TKV)r1;
+            qM[o] = (TKV)y0;
+            qM[o + 32] = (TKV)y1;
           }
-        }
-    } else {
-      const bool isk = head < hq + hkv;
-      const int kvh = isk ? head - hq : head - hq - hkv;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = rb + 32 * i + 8 * (e >> 2) + (e & 3);
-          float y0 = a0[i][e] * scale, y1 = a1[i][e] * scale;
-          const int p = row_pos[row];
-          if (isk) {
-            const float2 cs = rope[(size_t)p * 32 + c];
-            const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
-            y0 = r0;
-            y1 = r1;
-          }
-          const int page = page_table[(size_t)row_stream[row] * L.max_pages + p / kPage];
-          TKV* dst = kv + L.head_tile(layer, page, isk ? 0 : 1, kvh) + (p % kPage) * 64 + c;
+        } else {
+          TKV* dst = kv + L.head_tile(layer, pg[e], isk ? 0 : 1, kvh) + (p[e] % kPage) * 64 + c;
           dst[0] = (TKV)y0;
           dst[32] = (TKV)y1;
         }
+      }
     }
   }
   __device__ void operator()(const float* Cs, int ldc, int m0, int M, int n0, int BM, int BN) const {
-    const int nh = BN / 64;
-    for (int idx = threadIdx.x; idx < BM * 32 * nh; idx += blockDim.x) {
-      const int r = idx / (32 * nh), hh = (idx / 32) % nh, i = idx & 31, row = m0 + r;
-      const int head = n0 / 64 + hh;
-      if (row >= M || head >= hq + 2 * hkv) continue;
-      head_pair(row, head, i, Cs[r * ldc + hh * 64 + i], Cs[r * ldc + hh * 64 + i + 32]);
+    // Each row's position and KV page are looked up once per tile and kept
+    // in the row's padding of the tile (ldc >= BN + 2): the element loop
+    // then has no chain of dependent global loads per element.
+    int* info = const_cast<int*>(reinterpret_cast<const int*>(Cs));
+    for (int r = threadIdx.x; r < BM; r += blockDim.x) {
+      const int row = m0 + r;
+      if (row < M) {
+        const int p = row_pos[row];
+        info[r * ldc + BN] = p;
+        info[r * ldc + BN + 1] = page_table[(size_t)row_stream[row] * L.max_pages + p / kPage];
+      }
+    }
+    __syncthreads();
+    // U pairs per thread at a time: their rotations are loaded before any
+    // of their stores.
+    constexpr int U = 8;
+    const int nh = BN / 64, total = BM * 32 * nh;
+    for (int base = threadIdx.x; base < total; base += U * (int)blockDim.x) {
+      float2 cs[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = base + u * (int)blockDim.x;
+        const int r = idx / (32 * nh), head = n0 / 64 + (idx / 32) % nh;
+        cs[u] = make_float2(1.f, 0.f);
+        if (idx < total && m0 + r < M && head < hq + hkv) cs[u] = rope[(size_t)info[r * ldc + BN] * 32 + (idx & 31)];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = base + u * (int)blockDim.x;
+        const int r = idx / (32 * nh), hh = (idx / 32) % nh, i = idx & 31, row = m0 + r;
+        const int head = n0 / 64 + hh;
+        if (idx >= total || row >= M || head >= hq + 2 * hkv) continue;
+        head_pair_cs(row, head, i, Cs[r * ldc + hh * 64 + i], Cs[r * ldc + hh * 64 + i + 32], info[r * ldc + BN],
+                     info[r * ldc + BN + 1], cs[u]);
+      }
     }
   }
 };
@@ -940,9 +979,9 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
   // Measured on the 1B prompt shapes (d 2048, FFN 8192): gate/up at 1024 rows
   // takes 256 x 128 tiles (512 tiles, two rounds of the CUs; TTFT 3.74 ->
   // 3.44 ms against 256 x 256, one tile per CU); the down and O projections
-  // (only 128 tiles of 128 x 128) gain most from a 2-way K split; QKV, and
-  // everything at 256 rows, stay on the small-tile kernel, whose two
-  // workgroups per CU suit these few-tile shapes better.
+  // (only 128 tiles of 128 x 128) gain most from a 2-way K split; everything
+  // at 256 rows stays on the small-tile kernel, whose two workgroups per CU
+  // suit these few-tile shapes better.
   if (kind == GemmKind::GateUp && n_cols >= 8192) {
     // Eight waves (two per SIMD) here: TTFT at 1024 rows 3.66 -> 3.57 ms;
     // every other shape was slower with eight.
@@ -950,6 +989,10 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
     if (M >= 256) return WideCfg{128, 128, 1, 4};
   }
   if (kind == GemmKind::Resid && M >= 512) return WideCfg{128, 128, 2, 4};
+  // QKV at >= 512 rows: 128 x 128 tiles, no split (its epilogue loads its
+  // rotations and KV pages ahead of the stores): TTFT at 1024 rows 3.41 ->
+  // 3.34 ms against the small-tile kernel, which stays better at 256 rows.
+  if (kind == GemmKind::QKV && M >= 512) return WideCfg{128, 128, 1, 4};
   return WideCfg{0, 0, 1, 4};
 }
 

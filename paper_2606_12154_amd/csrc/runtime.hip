@@ -227,7 +227,9 @@ struct hh_ctx {
   unsigned step_count = 0;  // persistent-kernel launches so far (names each step's epochs)
   int device = 0;           // HIP device current at hh_create
   int step_depth = kStepLoadDepth;  // HH_LOAD_DEPTH: ring slots in flight per streaming wave
-  int step_quiet = 0;               // HH_STEP_QUIET: pause streaming during exchange waits
+  // HH_STEP_QUIET: pause streaming during exchange waits (1, the default:
+  // 0.657 -> 0.650 ms per token on the bench request; 0 streams through).
+  int step_quiet = 1;
   int step_ring = kStepRingSlots;   // HH_RING_SLOTS: LDS ring slots used (at most kStepRingSlots)
   int step_poll_delay = 60;         // HH_POLL_DELAY: 10 ns ticks before a phase's first exchange poll
   unsigned long long step_wait_ticks = 0;  // HH_STEP_WAIT_TICKS: wait limit (10 ns ticks; 0: 1 s), and

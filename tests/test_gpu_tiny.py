@@ -247,7 +247,7 @@ def test_stale_arena_contents(tiny):
 
 
 @pytest.mark.parametrize("var,value", [("HH_RING_SLOTS", "6"), ("HH_LOAD_DEPTH", "1"), ("HH_LOAD_DEPTH", "7"),
-                                       ("HH_STEP_QUIET", "1"), ("HH_STEP_QUIET", "2"), ("HH_POLL_DELAY", "0"),
+                                       ("HH_STEP_QUIET", "0"), ("HH_STEP_QUIET", "2"), ("HH_POLL_DELAY", "0"),
                                        ("HH_POLL_DELAY", "400")])
 def test_step_schedule_variants(tiny, var, value):
     """The single-kernel decode step's schedule settings (ring slots, loads
