@@ -8,6 +8,19 @@
 
 namespace hh {
 
+// Lockstep decode rows (one row per stream) whose QKV product was left as
+// K-split partials: the attention kernel sums them, scales, rotates q and k,
+// appends k and v to the cache and attends with them.  part == nullptr: q is
+// already rotated in q[] and the cache holds the row's key and value.
+template <typename TKV>
+struct QkvFold {
+  const float* part = nullptr;  // [splits][rows][ncols] fp32, ncols = (hq + 2 hkv) * 64
+  int splits = 0, ncols = 0;
+  float scale = 1.f;            // factor of the summed products (weight scale)
+  const float2* rope = nullptr; // (cos, sin) at [position][pair]
+  TKV* kv = nullptr;            // the cache (written at each row's position)
+};
+
 template <typename TW, typename TKV, typename TM>
 struct DecodeKernels {
   static void prep_embed(hipStream_t st, int n_rows, int prefill_stream, const int* feed, int* row_stream,
@@ -26,7 +39,7 @@ struct DecodeKernels {
                         float* part, float* o32, TM* oM);
   static void attention_rows(hipStream_t st, int n_rows, const float* q, const TKV* kv, KvLayout L, int layer,
                              const int* page_table, const int* row_stream, const int* row_pos, int hq, int hkv,
-                             float* o32, TM* oM);
+                             float* o32, TM* oM, const QkvFold<TKV>& fold = QkvFold<TKV>());
   static void rmsnorm_rows(hipStream_t st, int n_rows, const float* x, const float* gain, float eps, int d, TM* h);
 };
 
@@ -51,6 +64,12 @@ struct GemmKernels {
   static void qkv(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv, float scale,
                   const int* row_stream, const int* row_pos, const float2* rope, float* q, TM* qM, TKV* kv,
                   KvLayout L, int layer, const int* page_table, const TM* Wt = nullptr);
+  // The same product for lockstep decode rows with the split-K reduction
+  // left to the attention kernel: returns the K splits (partials in ws.ptr
+  // when > 1, nothing written yet); 1: the epilogue ran as in qkv().
+  static int qkv_deferred(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv,
+                          float scale, const int* row_stream, const int* row_pos, const float2* rope, float* q, TKV* kv,
+                          KvLayout L, int layer, const int* page_table, const TM* Wt = nullptr);
   // x += A W^T * scale; with gain, then h = rmsnorm(x) * gain (fused into the
   // split-K reduction when K is split).  Requires norm_fusable(N) with gain.
   static void resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x,

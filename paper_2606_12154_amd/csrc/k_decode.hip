@@ -471,7 +471,7 @@ struct KvPage {
 };
 
 template <typename TKV>
-__device__ __forceinline__ void kv_page_load(KvPage<TKV>& P, const TKV* __restrict__ kv, const KvLayout& L, int layer,
+__device__ __forceinline__ void kv_page_load(KvPage<TKV>& P, const TKV* kv, const KvLayout& L, int layer,
                                              int page, int g, int key, int quarter) {
   const u32x4* Kp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 0, g) + key * 64 + quarter * 16);
   const u32x4* Vp = reinterpret_cast<const u32x4*>(kv + L.head_tile(layer, page, 1, g) + key * 64 + quarter * 16);
@@ -482,27 +482,100 @@ __device__ __forceinline__ void kv_page_load(KvPage<TKV>& P, const TKV* __restri
   }
 }
 
+// kv is not __restrict__: with the QKV fold the kernel also writes the cache
+// (through fold.kv) at each row's position.
 template <typename TKV, typename TM, int G>
-__global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, const TKV* __restrict__ kv, KvLayout L,
+__global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, const TKV* kv, KvLayout L,
                                                    int layer, const int* __restrict__ page_table,
                                                    const int* __restrict__ row_stream, const int* __restrict__ row_pos,
-                                                   int hq, float* __restrict__ o32, TM* __restrict__ oM) {
-  constexpr int NW = 8;
+                                                   int hq, float* __restrict__ o32, TM* __restrict__ oM,
+                                                   QkvFold<TKV> fold) {
+  constexpr int NW = 8, NT = NW * 64;
   constexpr int SLOT = 66;  // m, l, o[64]
   __shared__ float st[NW * G * 4 * SLOT];
   __shared__ int pts[kRowsMaxPages];
+  // Folded QKV: this row's q heads g G .. g G + G - 1, then k and v of head
+  // g (64 values each), and the new key and value as the cache stores them.
+  __shared__ float qkv_s[(G + 2) * 64];
+  __shared__ TKV new_kv[2][64];
   const int g = blockIdx.x, r = blockIdx.y;
-  const int s = row_stream[r], t = row_pos[r] + 1, npg = (t + kPage - 1) / kPage;
+  const int s = row_stream[r], p = row_pos[r], t = p + 1, npg = (t + kPage - 1) / kPage;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, key = lane >> 2, quarter = lane & 3;
   const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
-  for (int i = threadIdx.x; i < npg && i < kRowsMaxPages; i += 512) pts[i] = page_table[(size_t)s * L.max_pages + i];
+  for (int i = threadIdx.x; i < npg && i < kRowsMaxPages; i += NT) pts[i] = page_table[(size_t)s * L.max_pages + i];
   auto page_of = [&](int pg) { return pg < kRowsMaxPages ? pts[pg] : page_table[(size_t)s * L.max_pages + pg]; };
+  const bool folded = fold.part != nullptr;
+  // Pages wave, wave + 8, ...: the next two pages' K/V are in flight while
+  // one is taken (three register sets in rotation); loads past the end
+  // re-read the row's last page.  The first two are issued before the folded
+  // QKV reduction, whose loads they overlap (the row's own key, which the
+  // reduction writes, is taken from LDS, not from these loads).
+  KvPage<TKV> A, B, C;
+  if (!folded) __syncthreads();  // pts
+  if (wave < npg) {
+    kv_page_load(A, kv, L, layer, folded ? page_table[(size_t)s * L.max_pages + wave] : page_of(wave), g, key, quarter);
+    const int pg1 = min(wave + NW, npg - 1);
+    kv_page_load(B, kv, L, layer, folded ? page_table[(size_t)s * L.max_pages + pg1] : page_of(pg1), g, key, quarter);
+  }
   float qv[G][16];
+  if (!folded) {
 #pragma unroll
-  for (int h = 0; h < G; ++h)
+    for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) qv[h][e] = q[((size_t)r * hq + g * G + h) * 64 + quarter * 16 + e] * qscale;
-  __syncthreads();
+      for (int e = 0; e < 16; ++e) qv[h][e] = q[((size_t)r * hq + g * G + h) * 64 + quarter * 16 + e] * qscale;
+  } else {
+    // Sum the split partials of the row's columns in split order and scale
+    // them (the reduction the QKV epilogue would otherwise run).
+    const int hkv = hq / G;
+    const size_t stride = (size_t)gridDim.y * fold.ncols;
+    for (int c = threadIdx.x; c < (G + 2) * 64; c += NT) {
+      const int col = c < G * 64 ? g * G * 64 + c
+                                 : (c < (G + 1) * 64 ? (hq + g) * 64 + (c - G * 64) : (hq + hkv + g) * 64 + (c - (G + 1) * 64));
+      const float* pp = fold.part + (size_t)r * fold.ncols + col;
+      float v = 0.f;
+      // Eight partials in flight at a time (clamped indices, extras unused).
+      for (int s0 = 0; s0 < fold.splits; s0 += 8) {
+        float u[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) u[j] = pp[min(s0 + j, fold.splits - 1) * stride];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (s0 + j < fold.splits) v += u[j];
+      }
+      qkv_s[c] = v * fold.scale;
+    }
+    __syncthreads();  // pts, qkv_s
+
+    // Rotary pairs (i, i + 32) of the q heads and of k; k and v go to the
+    // cache at position p and, as stored, to new_kv for this row's own key.
+    for (int i = threadIdx.x; i < (G + 2) * 32; i += NT) {
+      const int hh = i >> 5, e = i & 31;
+      float y0 = qkv_s[hh * 64 + e], y1 = qkv_s[hh * 64 + e + 32];
+      if (hh <= G) {
+        const float2 cs = fold.rope[(size_t)p * 32 + e];
+        const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+        y0 = r0;
+        y1 = r1;
+      }
+      if (hh < G) {
+        qkv_s[hh * 64 + e] = y0;
+        qkv_s[hh * 64 + e + 32] = y1;
+      } else {
+        const int kind = hh - G;
+        const TKV a = (TKV)y0, b = (TKV)y1;
+        new_kv[kind][e] = a;
+        new_kv[kind][e + 32] = b;
+        TKV* dst = fold.kv + L.head_tile(layer, page_of(p / kPage), kind, g) + (p % kPage) * 64;
+        dst[e] = a;
+        dst[e + 32] = b;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) qv[h][e] = qkv_s[h * 64 + quarter * 16 + e] * qscale;
+  }
 
   float m[G], lsum[G], o[G][16];
 #pragma unroll
@@ -520,6 +593,15 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       widen16(P.v[c], vf + c * Vec16<TKV>::n, TKV());
     }
     const bool valid = pg * kPage + key < t;
+    // With the QKV fold the row's own key and value come from LDS (the
+    // cache write above may not be visible to this wave's loads yet).
+    if (folded && pg * kPage + key == p) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        kf[e] = (float)new_kv[0][quarter * 16 + e];
+        vf[e] = (float)new_kv[1][quarter * 16 + e];
+      }
+    }
     // Slots past the stream's length hold stale data (possibly non-finite bit
     // patterns): their weight is 0, and 0 * NaN would be NaN.
 #pragma unroll
@@ -545,13 +627,7 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       m[h] = mn;
     }
   };
-  // Pages wave, wave + 8, ...: the next two pages' K/V are in flight while
-  // one is taken (three register sets in rotation); loads past the end
-  // re-read the row's last page.
   if (wave < npg) {
-    KvPage<TKV> A, B, C;
-    kv_page_load(A, kv, L, layer, page_of(wave), g, key, quarter);
-    kv_page_load(B, kv, L, layer, page_of(min(wave + NW, npg - 1)), g, key, quarter);
     for (int pg = wave; pg < npg; pg += 3 * NW) {
       kv_page_load(C, kv, L, layer, page_of(min(pg + 2 * NW, npg - 1)), g, key, quarter);
       take(A, pg);
@@ -682,13 +758,14 @@ void DecodeKernels<TW, TKV, TM>::attention(hipStream_t st, int n_rows, const flo
 template <typename TW, typename TKV, typename TM>
 void DecodeKernels<TW, TKV, TM>::attention_rows(hipStream_t st, int n_rows, const float* q, const TKV* kv,
                                                 KvLayout L, int layer, const int* page_table, const int* row_stream,
-                                                const int* row_pos, int hq, int hkv, float* o32, TM* oM) {
+                                                const int* row_pos, int hq, int hkv, float* o32, TM* oM,
+                                                const QkvFold<TKV>& fold) {
   const dim3 grid(hkv, n_rows);
   switch (hq / hkv) {
-    case 1: k_attn_rows<TKV, TM, 1><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
-    case 2: k_attn_rows<TKV, TM, 2><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
-    case 4: k_attn_rows<TKV, TM, 4><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
-    default: k_attn_rows<TKV, TM, 8><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM); break;
+    case 1: k_attn_rows<TKV, TM, 1><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM, fold); break;
+    case 2: k_attn_rows<TKV, TM, 2><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM, fold); break;
+    case 4: k_attn_rows<TKV, TM, 4><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM, fold); break;
+    default: k_attn_rows<TKV, TM, 8><<<grid, 512, 0, st>>>(q, kv, L, layer, page_table, row_stream, row_pos, hq, o32, oM, fold); break;
   }
 }
 

@@ -314,8 +314,18 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv, c->cfg.max_context);
       // Flash attention reads only the fp16 queries.
       const bool tiled = !L.wqkvT16.empty();
-      GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, flash ? nullptr : q,
-              flash ? c->at<TM>(L.qM) : nullptr, kv, kl, l, pt, tiled ? c->at<TM>(L.wqkvT16[l]) : nullptr);
+      // Lockstep decode rows (one per stream): the attention kernel takes
+      // over the QKV split-K reduction, rotation and KV append.
+      const bool fold = prefill_stream < 0 && head_row == -1;
+      QkvFold<TKV> qf;
+      if (fold) {
+        const int sp = GK::qkv_deferred(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, kv, kl, l,
+                                        pt, tiled ? c->at<TM>(L.wqkvT16[l]) : nullptr);
+        if (sp > 1) qf = QkvFold<TKV>{gws.ptr, sp, (hq + 2 * hkv) * 64, ws, rope, kv};
+      } else {
+        GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, flash ? nullptr : q,
+                flash ? c->at<TM>(L.qM) : nullptr, kv, kl, l, pt, tiled ? c->at<TM>(L.wqkvT16[l]) : nullptr);
+      }
       if (flash) {
         if constexpr (sizeof(TKV) == 2)
           flash_prefill(st, reinterpret_cast<const _Float16*>(c->at<TM>(L.qM)), reinterpret_cast<const _Float16*>(kv),
@@ -323,7 +333,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       } else if (prefill_stream >= 0) {
         DK::attention(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, 1, c->at<float>(L.part), o32, oM);
       } else {
-        DK::attention_rows(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, o32, oM);
+        DK::attention_rows(st, n, q, kv, kl, l, pt, rs, rp, hq, hkv, o32, oM, qf);
       }
       const TM* wo_t = tiled ? c->at<TM>(L.woT16[l]) : nullptr;
       if (fuse) {
