@@ -84,7 +84,9 @@ struct GemmKernels {
 };
 
 // ---- causal flash attention for prefill rows of one stream (k_attn_prefill.hip)
-bool flash_prefill_supported(int G, int max_context);
+// layer_kv_elems: K and V elements of one layer's cache (the kernel's
+// offsets are 32-bit).
+bool flash_prefill_supported(int G, int max_context, size_t layer_kv_elems);
 void flash_prefill(hipStream_t st, const _Float16* qM, const _Float16* kv, KvLayout L, int layer,
                    const int* page_table, int s, int p0, int n_rows, int hq, int hkv, _Float16* oM);
 

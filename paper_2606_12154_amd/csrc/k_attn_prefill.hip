@@ -25,26 +25,41 @@ constexpr int kFlashMaxPages = 8192;  // pages of keys per prefill attention (13
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+// Thread idx of a group stages, of the block's 32 keys,
+//   K: key idx / 8, dims 8 (idx % 8) .. + 8 (a wave reads 8 whole 128-byte rows);
+//   V: key idx % 32, dims 8 (idx / 32) .. + 8, so a wave's transposed V^T
+//      stores (one half per lane and dim) cover all 32 keys of two dim chunks
+//      and spread over every LDS bank instead of piling onto four.
 struct KvRegs {
-  f16x8 k, v;  // key idx / 8 of the block, dims (idx % 8) * 8 .. + 8, for this thread's idx
+  f16x8 k, v;
 };
 
 // pt: the stream's page-table slice in LDS (a global read here would make
 // every prefetch wait, in order, for all loads before it).  idx: the thread's
 // index within its group (0 .. 255 stage a block).
-__device__ __forceinline__ void flash_load(KvRegs& R, const _Float16* __restrict__ kv, const KvLayout& L, int layer,
-                                           const int* pt, int g, int idx, int k0, int kend) {
-  const int key = min(k0 + (idx >> 3), kend - 1), dc = idx & 7;
-  const size_t off = (size_t)(key & 15) * 64 + dc * 8;
-  const int page = pt[key >> 4];
-  R.k = *reinterpret_cast<const f16x8*>(kv + L.head_tile(layer, page, 0, g) + off);
-  R.v = *reinterpret_cast<const f16x8*>(kv + L.head_tile(layer, page, 1, g) + off);
+// Keys of kv head g in one layer, addressed with 32-bit element offsets from
+// the head's first tile (flash_prefill_supported bounds a layer's cache).
+struct FlashKv {
+  const _Float16* base;   // head_tile(layer, 0, 0, g)
+  unsigned page_stride;   // elements between pages: 2 (K, V) x heads x one tile
+  unsigned v_off;         // V tile of a page after its K tile
+};
+__device__ __forceinline__ void flash_load(KvRegs& R, const FlashKv& A, const int* pt, int idx, int k0, int kend) {
+  const int kk = min(k0 + (idx >> 3), kend - 1), kd = idx & 7;
+  const int vk = min(k0 + (idx & 31), kend - 1), vd = idx >> 5;
+  const unsigned ko = (unsigned)pt[kk >> 4] * A.page_stride + (unsigned)((kk & 15) * 64 + kd * 8);
+  const unsigned vo = (unsigned)pt[vk >> 4] * A.page_stride + A.v_off + (unsigned)((vk & 15) * 64 + vd * 8);
+  R.k = *reinterpret_cast<const f16x8*>(A.base + ko);
+  R.v = *reinterpret_cast<const f16x8*>(A.base + vo);
 }
 
 template <int G, int NS>
 struct FlashCfg {
   static constexpr int THREADS = 64 * G * NS;
-  static constexpr int VT_LD = 32 + 8;                 // padded row of V^T (halfs)
+  // Padded row of V^T (halfs): 18 banks per row, so the two dim chunks of a
+  // wave's transposed stores (rows 8 apart) fall 16 banks apart, and the
+  // fragment reads (8 bytes, rows c = 0..31) cover every bank equally.
+  static constexpr int VT_LD = 32 + 4;
   static constexpr int KT_LD = 64 + 8;                 // padded row of K (halfs)
   static constexpr int BUF = (64 * VT_LD + 32 * KT_LD) * 2;  // one staged key block, bytes
   static constexpr int STAGE = NS * 2 * BUF;           // double-buffered, per group
@@ -71,6 +86,12 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int hi = wave % G, grp = wave / G;
   const int idx = threadIdx.x - grp * 64 * G;  // thread index within the group
+  // Threads 0..255 of a group load and stage its key blocks.  With 256-thread
+  // groups that is every thread, and the condition must be visibly true:
+  // loads under a runtime branch make the compiler's wait counts assume the
+  // branch skipped them, so each block's wait would also wait for the next
+  // block's loads.
+  const bool stager = G * 64 == 256 || idx < 256;
   const int j = g * G + hi;
   const int h = lane >> 5, c = lane & 31;
   const int qrow = q0 + c;
@@ -94,11 +115,30 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   const int kend = min(p0 + q0 + 32, p0 + n_rows);  // keys 0 .. kend-1 exist for this block
   const int nkb = (kend + 31) / 32;
   const int niter = (nkb + NS - 1) / NS;            // the same for every group (uniform barriers)
+  // Arrival counters of the NS groups' per-iteration barriers.
+  __shared__ int gsync[NS];
+  if (threadIdx.x < NS) gsync[threadIdx.x] = 0;
   {
     const int* src = page_table + (size_t)s * L.max_pages;
     for (int i = threadIdx.x; i < (kend + kPage - 1) / kPage; i += blockDim.x) pt[i] = src[i];
     __syncthreads();
   }
+  // Barrier among the G waves of this thread's group only: groups share no
+  // staging buffer, so each runs at its own pace and a SIMD (one wave of
+  // every group) overlaps one group's MFMAs with another's softmax instead of
+  // running them in lock step.  The arrival is counted once this wave's LDS
+  // stores have completed; the wait is bounded (it cannot miss in a correct
+  // run: every wave of a group arrives once per iteration).
+  auto group_sync = [&](int it) {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's staging stores are done
+    if (lane == 0) __hip_atomic_fetch_add(&gsync[grp], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const int target = G * (it + 1);
+    for (int spin = 0; spin < (1 << 24); ++spin) {
+      if (__hip_atomic_load(&gsync[grp], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= target) break;
+      __builtin_amdgcn_s_sleep(1);
+    }
+    asm volatile("" ::: "memory");  // the staged block is read only after the wait
+  };
 
   char* gbase = smem + grp * 2 * C::BUF;
   auto process = [&](const KvRegs& R, int it) {
@@ -107,18 +147,18 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     const bool have = kb < nkb;
     _Float16* vb = reinterpret_cast<_Float16*>(gbase + (it & 1) * C::BUF);
     _Float16* kbuf = vb + 64 * C::VT_LD;
-    // Stage K and V^T of this key block once for the group's waves (group
-    // threads 0..255: key idx / 8, dims (idx % 8) * 8 .. + 8).
-    if (have && idx < 256) {
-      const int key = idx >> 3, dc = idx & 7;
-      const bool ok = k0 + key < kend;
-      *reinterpret_cast<f16x8*>(kbuf + key * C::KT_LD + dc * 8) = R.k;
+    // Stage K and V^T of this key block once for the group's waves (the
+    // thread-to-key maps of flash_load).
+    if (have && stager) {
+      *reinterpret_cast<f16x8*>(kbuf + (idx >> 3) * C::KT_LD + (idx & 7) * 8) = R.k;
+      const int vk = idx & 31, vd = idx >> 5;
+      const bool ok = k0 + vk < kend;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) vb[(dc * 8 + e) * C::VT_LD + key] = ok ? R.v[e] : (_Float16)0.f;
+      for (int e = 0; e < 8; ++e) vb[(vd * 8 + e) * C::VT_LD + vk] = ok ? R.v[e] : (_Float16)0.f;
     }
     // Buffers alternate, so one barrier per iteration orders this write
     // after every read of the same buffer two iterations ago.
-    __syncthreads();
+    group_sync(it);
     if (!have) return;
 
     f32x16 sacc;
@@ -130,36 +170,50 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[ks], sacc, 0, 0, 0);
     }
 
+    // The softmax is the VALU side of the loop (four waves per SIMD share it
+    // while the MFMAs are short), so it does only what a block needs: keys
+    // past a query (causal) or past the block's end exist only in blocks
+    // that reach the diagonal (wave-uniform test), the scale folds into the
+    // exponent's FMA (the max is taken on raw scores: scaling by a positive
+    // factor keeps the order), and a query's reference m moves only when
+    // the block's max exceeds it by more than kLazy (log2 units), so the
+    // output is rescaled in few blocks (alpha is exactly 1 otherwise).
+    // Weights are then at most 2^kLazy, which fp16 holds with its full
+    // relative precision; the final (m, l, o) stay consistent.
+    if (k0 + 31 > p0 + q0 || k0 + 32 > kend) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int kk = k0 + 8 * (i >> 2) + 4 * h + (i & 3);
+        if (kk > qpos || kk >= kend) sacc[i] = -INFINITY;
+      }
+    }
     float bm = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int kk = k0 + 8 * (i >> 2) + 4 * h + (i & 3);
-      float v = sacc[i] * scale;
-      if (kk > qpos || kk >= kend) v = -INFINITY;
-      sacc[i] = v;
-      bm = fmaxf(bm, v);
-    }
-    bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+    for (int i = 0; i < 16; ++i) bm = fmaxf(bm, sacc[i]);
+    bm = fmaxf(bm, __shfl_xor(bm, 32, 64)) * scale;
     // A group's first blocks may hide every key from some query of an
     // appended chunk: keep such a query's state at (-inf, 0, 0).
-    const float mn = fmaxf(m, bm);
+    constexpr float kLazy = 8.f;
+    const float mn = bm > m + kLazy ? bm : m;  // m = -inf: any finite bm
     const float mref = mn == -INFINITY ? 0.f : mn;
-    // Hardware exp2 (arguments are <= 0; results below the normal range flush
-    // to zero, which a softmax weight can take).
+    // Hardware exp2 (arguments are <= 0 up to the product's rounding; results
+    // below the normal range flush to zero, which a softmax weight can take).
     const float alpha = __builtin_amdgcn_exp2f(m - mref);
     float ls = 0.f;
     f16x8 pb[2];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float pv = __builtin_amdgcn_exp2f(sacc[i] - mref);
+      const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[i], scale, -mref));
       ls += pv;
       pb[i >> 3][i & 7] = (_Float16)pv;
     }
     lsum = lsum * alpha + ls;
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      o0[i] *= alpha;
-      o1[i] *= alpha;
+      for (int i = 0; i < 16; ++i) {
+        o0[i] *= alpha;
+        o1[i] *= alpha;
+      }
     }
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
@@ -184,20 +238,22 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   // while block it is processed (loads of absent blocks are clamped, never
   // used).
   KvRegs R0, R1, R2;
+  const FlashKv fkv{kv + L.head_tile(layer, 0, 0, g), (unsigned)(2 * L.n_kv_heads * kPage * kHeadDim),
+                    (unsigned)(L.n_kv_heads * kPage * kHeadDim)};
   const int kcl = (nkb - 1) * 32;
   auto blk = [&](int it) { return min((it * NS + grp) * 32, kcl); };
-  if (idx < 256) {
-    flash_load(R0, kv, L, layer, pt, g, idx, blk(0), kend);
-    flash_load(R1, kv, L, layer, pt, g, idx, blk(1), kend);
+  if (stager) {
+    flash_load(R0, fkv, pt, idx, blk(0), kend);
+    flash_load(R1, fkv, pt, idx, blk(1), kend);
   }
   for (int it = 0; it < niter; it += 3) {
-    if (idx < 256) flash_load(R2, kv, L, layer, pt, g, idx, blk(it + 2), kend);
+    if (stager) flash_load(R2, fkv, pt, idx, blk(it + 2), kend);
     process(R0, it);
     if (it + 1 >= niter) break;
-    if (idx < 256) flash_load(R0, kv, L, layer, pt, g, idx, blk(it + 3), kend);
+    if (stager) flash_load(R0, fkv, pt, idx, blk(it + 3), kend);
     process(R1, it + 1);
     if (it + 2 >= niter) break;
-    if (idx < 256) flash_load(R1, kv, L, layer, pt, g, idx, blk(it + 4), kend);
+    if (stager) flash_load(R1, fkv, pt, idx, blk(it + 4), kend);
     process(R2, it + 2);
   }
   lsum += __shfl_xor(lsum, 32, 64);
@@ -253,8 +309,9 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   }
 }
 
-bool flash_prefill_supported(int G, int max_context) {
-  return (G == 4 || G == 8) && (max_context + kPage - 1) / kPage <= kFlashMaxPages;
+bool flash_prefill_supported(int G, int max_context, size_t layer_kv_elems) {
+  return (G == 4 || G == 8) && (max_context + kPage - 1) / kPage <= kFlashMaxPages &&
+         layer_kv_elems <= 0xFFFFFFFFull;
 }
 
 template <int G, int NS>

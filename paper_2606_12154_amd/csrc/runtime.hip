@@ -311,7 +311,9 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       if (!fuse) DK::rmsnorm_rows(st, n, x, an, eps, d, h);
       else if (l == 0) GK::rmsnorm(st, n, x, d, an, eps, h);
       // Prefill rows of one stream with an fp16 cache use MFMA flash attention.
-      const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 && flash_prefill_supported(hq / hkv, c->cfg.max_context);
+      const bool flash = prefill_stream >= 0 && sizeof(TKV) == 2 &&
+                         flash_prefill_supported(hq / hkv, c->cfg.max_context,
+                                                 (size_t)kl.n_pages * 2 * hkv * kPage * kHeadDim);
       // Flash attention reads only the fp16 queries.
       const bool tiled = !L.wqkvT16.empty();
       // Lockstep decode rows (one per stream): the attention kernel takes
