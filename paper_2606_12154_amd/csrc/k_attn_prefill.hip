@@ -1,10 +1,12 @@
 // Causal GQA flash attention for prompt prefill on gfx950 MFMA (fp16 KV).
 //
-// A workgroup owns one block of 32 query positions and one kv head g.  Its
-// waves form NS key-split groups of G waves; wave w of a group serves query
-// head g * G + w, and group s takes key blocks s, s + NS, s + 2 NS, ... of 32
-// keys (two KV pages), so the longest dependency chain is 1/NS of the keys and
-// every SIMD runs four waves that hide each other's latencies.  Per key block:
+// A workgroup owns two blocks of 32 query positions, p and the mirror block
+// from the end (so every workgroup has the same causal work), and half of kv
+// head g's query heads.  Its waves form NS key-split groups of G waves; a
+// group's waves serve (query block, head) pairs, and group s takes key blocks
+// s, s + NS, s + 2 NS, ... of 32 keys (two KV pages) of the longer block, so
+// the longest dependency chain is 1/NS of the keys and every SIMD runs four
+// waves that hide each other's latencies.  Per key block:
 //   S^T[key][query] = K[key][:] . Q[query][:]      4 x mfma_f32_32x32x16_f16
 // so a lane holds 16 keys of ONE query column (lane % 32), and the row max /
 // sum of the online softmax need a single exchange with lane ^ 32.  Then
@@ -80,11 +82,23 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   using C = FlashCfg<G, NS>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int* pt = reinterpret_cast<int*>(smem + (C::LDS - C::PT));  // physical pages of keys 0 .. kend-1
-  const int g = blockIdx.y;
-  const int qb = gridDim.x - 1 - blockIdx.x;  // longest (latest) query blocks first
-  const int q0 = qb * 32;
+  // Causal work is balanced by pairing query blocks: workgroup (p, g, hh)
+  // serves query blocks p and nqb - 1 - p (together nqb + 1 key blocks, the
+  // same for every pair) for the query heads g G + hh G/2 .. + G/2 - 1.  In
+  // each group, waves 0 .. G/2 - 1 take one block and the others the second,
+  // alternating with the group index: a SIMD runs wave w of every group, so
+  // each SIMD gets waves of both blocks and none idles once the short block
+  // is done.
+  constexpr int GH = G / 2;  // query heads per workgroup
+  const int g = blockIdx.y, hh = blockIdx.z;
+  const int nqb = (n_rows + 31) / 32;
+  const int p = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int hi = wave % G, grp = wave / G;
+  const int qsel = ((hi / GH) + grp) & 1;                  // 0: block p, 1: block nqb - 1 - p
+  const int qb = qsel ? nqb - 1 - p : p;
+  const bool active = qsel == 0 || nqb - 1 - p != p;     // an odd count's middle block is served once
+  const int q0 = qb * 32;
   const int idx = threadIdx.x - grp * 64 * G;  // thread index within the group
   // Threads 0..255 of a group load and stage its key blocks.  With 256-thread
   // groups that is every thread, and the condition must be visibly true:
@@ -92,10 +106,10 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   // branch skipped them, so each block's wait would also wait for the next
   // block's loads.
   const bool stager = G * 64 == 256 || idx < 256;
-  const int j = g * G + hi;
+  const int j = g * G + hh * GH + hi % GH;
   const int h = lane >> 5, c = lane & 31;
   const int qrow = q0 + c;
-  const bool qvalid = qrow < n_rows;
+  const bool qvalid = active && qrow < n_rows;
   const int qpos = p0 + qrow;
   const float scale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
 
@@ -112,15 +126,19 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     o0[i] = 0.f;
     o1[i] = 0.f;
   }
-  const int kend = min(p0 + q0 + 32, p0 + n_rows);  // keys 0 .. kend-1 exist for this block
-  const int nkb = (kend + 31) / 32;
-  const int niter = (nkb + NS - 1) / NS;            // the same for every group (uniform barriers)
+  // This wave's query block sees keys 0 .. kend - 1; the workgroup stages
+  // key blocks for the longer block of the pair (keys 0 .. kend_all - 1).
+  const int kend = min(p0 + q0 + 32, p0 + n_rows);
+  const int nkb = active ? (kend + 31) / 32 : 0;
+  const int kend_all = min(p0 + (nqb - 1 - p) * 32 + 32, p0 + n_rows);
+  const int nkb_all = (kend_all + 31) / 32;
+  const int niter = (nkb_all + NS - 1) / NS;        // the same for every group (uniform barriers)
   // Arrival counters of the NS groups' per-iteration barriers.
   __shared__ int gsync[NS];
   if (threadIdx.x < NS) gsync[threadIdx.x] = 0;
   {
     const int* src = page_table + (size_t)s * L.max_pages;
-    for (int i = threadIdx.x; i < (kend + kPage - 1) / kPage; i += blockDim.x) pt[i] = src[i];
+    for (int i = threadIdx.x; i < (kend_all + kPage - 1) / kPage; i += blockDim.x) pt[i] = src[i];
     __syncthreads();
   }
   // Barrier among the G waves of this thread's group only: groups share no
@@ -144,15 +162,15 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   auto process = [&](const KvRegs& R, int it) {
     const int kb = it * NS + grp;
     const int k0 = kb * 32;
-    const bool have = kb < nkb;
+    const bool staged = kb < nkb_all, have = kb < nkb;
     _Float16* vb = reinterpret_cast<_Float16*>(gbase + (it & 1) * C::BUF);
     _Float16* kbuf = vb + 64 * C::VT_LD;
     // Stage K and V^T of this key block once for the group's waves (the
     // thread-to-key maps of flash_load).
-    if (have && stager) {
+    if (staged && stager) {
       *reinterpret_cast<f16x8*>(kbuf + (idx >> 3) * C::KT_LD + (idx & 7) * 8) = R.k;
       const int vk = idx & 31, vd = idx >> 5;
-      const bool ok = k0 + vk < kend;
+      const bool ok = k0 + vk < kend_all;
 #pragma unroll
       for (int e = 0; e < 8; ++e) vb[(vd * 8 + e) * C::VT_LD + vk] = ok ? R.v[e] : (_Float16)0.f;
     }
@@ -240,20 +258,20 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
   KvRegs R0, R1, R2;
   const FlashKv fkv{kv + L.head_tile(layer, 0, 0, g), (unsigned)(2 * L.n_kv_heads * kPage * kHeadDim),
                     (unsigned)(L.n_kv_heads * kPage * kHeadDim)};
-  const int kcl = (nkb - 1) * 32;
+  const int kcl = (nkb_all - 1) * 32;
   auto blk = [&](int it) { return min((it * NS + grp) * 32, kcl); };
   if (stager) {
-    flash_load(R0, fkv, pt, idx, blk(0), kend);
-    flash_load(R1, fkv, pt, idx, blk(1), kend);
+    flash_load(R0, fkv, pt, idx, blk(0), kend_all);
+    flash_load(R1, fkv, pt, idx, blk(1), kend_all);
   }
   for (int it = 0; it < niter; it += 3) {
-    if (stager) flash_load(R2, fkv, pt, idx, blk(it + 2), kend);
+    if (stager) flash_load(R2, fkv, pt, idx, blk(it + 2), kend_all);
     process(R0, it);
     if (it + 1 >= niter) break;
-    if (stager) flash_load(R0, fkv, pt, idx, blk(it + 3), kend);
+    if (stager) flash_load(R0, fkv, pt, idx, blk(it + 3), kend_all);
     process(R1, it + 1);
     if (it + 2 >= niter) break;
-    if (stager) flash_load(R1, fkv, pt, idx, blk(it + 4), kend);
+    if (stager) flash_load(R1, fkv, pt, idx, blk(it + 4), kend_all);
     process(R2, it + 2);
   }
   lsum += __shfl_xor(lsum, 32, 64);
@@ -275,9 +293,11 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     }
     __syncthreads();
     if (grp > 0) return;
+    // Group sp keeps this wave's (query block, head) at position hs(sp).
+    auto hs = [&](int sp) { return (((qsel + sp) & 1) * GH) + hi % GH; };
     float mx = m;
 #pragma unroll
-    for (int sp = 1; sp < NS; ++sp) mx = fmaxf(mx, mg[((sp - 1) * G + hi) * (2 + 32) * 64 + lane]);
+    for (int sp = 1; sp < NS; ++sp) mx = fmaxf(mx, mg[((sp - 1) * G + hs(sp)) * (2 + 32) * 64 + lane]);
     const float w0 = __builtin_amdgcn_exp2f(m - mx);
     lsum *= w0;
 #pragma unroll
@@ -287,7 +307,7 @@ __global__ __launch_bounds__(64 * G * NS) void k_flash_prefill(const _Float16* _
     }
 #pragma unroll
     for (int sp = 1; sp < NS; ++sp) {
-      const float* r = mg + ((sp - 1) * G + hi) * (2 + 32) * 64;
+      const float* r = mg + ((sp - 1) * G + hs(sp)) * (2 + 32) * 64;
       const float w = __builtin_amdgcn_exp2f(r[lane] - mx);  // 0 for a split that saw no key
       lsum += w * r[64 + lane];
 #pragma unroll
@@ -330,7 +350,8 @@ static void launch_flash(hipStream_t st, dim3 grid, const _Float16* qM, const _F
 void flash_prefill(hipStream_t st, const _Float16* qM, const _Float16* kv, KvLayout L, int layer,
                    const int* page_table, int s, int p0, int n_rows, int hq, int hkv, _Float16* oM) {
   const int G = hq / hkv;
-  dim3 grid((n_rows + 31) / 32, hkv);
+  // Pairs of query blocks x kv heads x two halves of each kv head's query heads.
+  dim3 grid(((n_rows + 31) / 32 + 1) / 2, hkv, 2);
   switch (G) {
     case 4: launch_flash<4, 4>(st, grid, qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM); break;
     default: launch_flash<8, 2>(st, grid, qM, kv, L, layer, page_table, s, p0, n_rows, hq, oM); break;
