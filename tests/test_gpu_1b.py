@@ -70,7 +70,7 @@ GEMM_KINDS = ("HH_GEMM_QKV", "HH_GEMM_RESID", "HH_GEMM_DOWN", "HH_GEMM_GATEUP")
 
 
 @pytest.mark.parametrize("tile", ["256x256x1", "256x128x1", "128x256x1", "128x128x1", "256x256x4", "128x128x2",
-                                  "256x256x1x8", "256x128x2x8", "128x256x1x8"])
+                                  "256x256x1x8", "256x128x2x8", "128x256x1x8", "128x128x1x8", "128x128x2x8"])
 @pytest.mark.parametrize("n", [256, 200])
 def test_prefill_wide_tiles(one_b, ctx, prompt_ref, tile, n):
     """Every large-tile GEMM shape (and split-K; four or eight waves per
