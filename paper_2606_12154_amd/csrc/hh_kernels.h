@@ -57,6 +57,27 @@ struct GemmWorkspace {
   size_t bytes;
 };
 
+// RMSNorm split across a residual product and the product that reads its
+// output, for the <= 32-row GEMMs: a row's norm factor is one scalar, so it
+// can scale the consumer's output rows instead of its input.
+//  * producer (a residual product whose K is split): the last split of each
+//    64-column block to finish adds the split sum (in split order) into x,
+//    writes y = x * gain (elementwise) as fp16 and the block's per-row sums
+//    of squares to ss_out[row * (N / 64) + block]; cnt holds one counter per
+//    column block, zero before and after every launch;
+//  * consumer: row r of A is such a y; the product's row r is scaled by
+//    rsqrt(sum over blocks of ss_in[r * nss + j] / n + eps) before its
+//    split partials or epilogue.
+struct RowNorm {
+  const float* ss_in = nullptr;
+  int nss = 0;
+  float n = 1.f, eps = 0.f;
+  int* cnt = nullptr;
+  const float* gain = nullptr;
+  _Float16* y = nullptr;
+  float* ss_out = nullptr;
+};
+
 template <typename TM, typename TKV>
 struct GemmKernels {
   // Wt (optional): the same matrix as 16 x 32 operand tiles (tile16), used
@@ -69,18 +90,24 @@ struct GemmKernels {
   // when > 1, nothing written yet); 1: the epilogue ran as in qkv().
   static int qkv_deferred(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq, int hkv,
                           float scale, const int* row_stream, const int* row_pos, const float2* rope, float* q, TKV* kv,
-                          KvLayout L, int layer, const int* page_table, const TM* Wt = nullptr);
+                          KvLayout L, int layer, const int* page_table, const TM* Wt = nullptr,
+                          const RowNorm& rn = RowNorm());
   // x += A W^T * scale; with gain, then h = rmsnorm(x) * gain (fused into the
   // split-K reduction when K is split).  Requires norm_fusable(N) with gain.
-  static void resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x,
-                    const float* gain = nullptr, float eps = 0.f, TM* h = nullptr, const TM* Wt = nullptr);
+  // With ss and cnt (RowNorm's producer buffers) the 32-row GEMM may instead
+  // leave h = x * gain and the row sums of squares in ss: returns true then,
+  // and the product reading h takes RowNorm{ss, N / 64, N, eps}.
+  static bool resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x,
+                    const float* gain = nullptr, float eps = 0.f, TM* h = nullptr, const TM* Wt = nullptr,
+                    float* ss = nullptr, int* cnt = nullptr);
   static bool norm_fusable(int N);
   // h = rmsnorm(x) * gain, one row per workgroup (norm_fusable(N)).
   static void rmsnorm(hipStream_t st, int M, float* x, int N, const float* gain, float eps, TM* h);
   static void gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale, TM* m,
-                     const TM* Wt = nullptr);
+                     const TM* Wt = nullptr, const RowNorm& rn = RowNorm());
   static void logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale, float* logits,
-                     unsigned long long* slot, const int* row_stream, const TM* Wt = nullptr);
+                     unsigned long long* slot, const int* row_stream, const TM* Wt = nullptr,
+                     const RowNorm& rn = RowNorm());
 };
 
 // ---- causal flash attention for prefill rows of one stream (k_attn_prefill.hip)

@@ -808,15 +808,167 @@ static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
 // B fragment reads conflict-free).  The finished 64-column tile goes through
 // LDS into the usual epilogue, or into split partials when K is split to give
 // every CU work.
+// RowNorm consumer: threads 0..127 each load 16 of a row's block sums of
+// squares (row t / 4, blocks t % 4 + 4 i; zeros past M rows or nss blocks,
+// so nss <= 64) early, so that the tail finds them landed.
+constexpr int kRowNormLoads = 16;
+__device__ __forceinline__ void row_norm_loads(float (&ssv)[kRowNormLoads], const RowNorm& rn, int M) {
+  if (!rn.ss_in || threadIdx.x >= 128) return;
+  const __amdgpu_buffer_rsrc_t res =
+      __builtin_amdgcn_make_buffer_rsrc((void*)rn.ss_in, (short)0, (int)((size_t)M * rn.nss * 4), 0x00020000);
+  const int r = threadIdx.x >> 2, part = threadIdx.x & 3;
+#pragma unroll
+  for (int i = 0; i < kRowNormLoads; ++i) {
+    const int j = part + 4 * i;
+    ssv[i] = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(res, j < rn.nss && r < M ? (unsigned)((r * rn.nss + j) * 4) : 0x80000000u,
+                                                    0, 0));
+  }
+}
+
+// acc0[j] of lane l: column 16 rw + 4 (l / 16) + j, row l % 16 (acc1: row
+// + 16).  K groups add into the LDS tile Cs (32 x 68 floats, which the caller's
+// activation buffer holds once every wave is done with it) in group order;
+// rows are scaled by their norm factors (RowNorm consumer), then the tile
+// goes to the split partials or through the epilogue.  A RowNorm producer's
+// last split of the column block then finishes the residual (rs, flag: LDS
+// scratch of 32 floats and one int).
+template <class Epi, int KW>
+__device__ __forceinline__ void skinny_tail(float* Cs, const f32x4& acc0, const f32x4& acc1, int rw, int kg, int lane,
+                                            float* __restrict__ partial, int split, int splits, int cb, int M,
+                                            int ncols, int n0, const Epi& epi, const RowNorm& rn,
+                                            const float (&ssv)[kRowNormLoads], float* rs, int* flag) {
+  constexpr int LDC = 68;
+  const int col = 16 * rw + 4 * (lane >> 4), r = lane & 15;
+  float f0 = 1.f, f1 = 1.f;  // norm factors of rows r and r + 16
+  if (rn.ss_in) {
+    if (threadIdx.x < 128) {
+      float v = 0.f;
+#pragma unroll
+      for (int i = 0; i < kRowNormLoads; ++i) v += ssv[i];
+      v += __shfl_xor(v, 1);
+      v += __shfl_xor(v, 2);
+      if ((threadIdx.x & 3) == 0) rs[threadIdx.x >> 2] = rsqrtf(v / rn.n + rn.eps);
+    }
+    __syncthreads();
+    f0 = rs[r];
+    f1 = rs[r + 16];
+  }
+#pragma unroll
+  for (int g = 0; g < KW; ++g) {
+    if (kg == g) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        Cs[r * LDC + col + j] = (g ? Cs[r * LDC + col + j] : 0.f) + acc0[j] * f0;
+        Cs[(r + 16) * LDC + col + j] = (g ? Cs[(r + 16) * LDC + col + j] : 0.f) + acc1[j] * f1;
+      }
+    }
+    __syncthreads();
+  }
+  if (partial) {
+    bool producer = false;
+    if constexpr (std::is_same<Epi, EpiResid>::value) producer = rn.cnt != nullptr;
+    if (!producer) {
+      float* dst = partial + (size_t)split * M * ncols;
+      for (int i = threadIdx.x; i < M * 64; i += blockDim.x) {
+        const int rr = i / 64, c = i % 64;
+        if (n0 + c < ncols) dst[(size_t)rr * ncols + n0 + c] = Cs[rr * LDC + c];
+      }
+      return;
+    }
+    if constexpr (std::is_same<Epi, EpiResid>::value) {
+      // RowNorm producer.  The partials go out and come back with the
+      // agent-coherent cache policy, so that no fence (and no writeback or
+      // invalidation of a whole L2) is needed: a split's stores have
+      // completed before it counts itself in, and the last split to arrive
+      // reads every split's partials from the coherent level.
+      constexpr int kSc1 = 16;
+      const int N = epi.N;
+      const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)partial, (short)0, (int)((size_t)splits * M * ncols * 4), 0x00020000);
+      const unsigned sstride = (unsigned)M * ncols * 4;  // bytes of one split's partials
+      for (int it = threadIdx.x; it < M * 16; it += blockDim.x) {
+        const int rr = it >> 4, c = n0 + 4 * (it & 15);
+        if (c < ncols) {
+          const float4 v = *reinterpret_cast<const float4*>(Cs + rr * LDC + 4 * (it & 15));
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), pres,
+                                                 (unsigned)split * sstride + (unsigned)(rr * ncols + c) * 4, 0, kSc1);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // every store of this thread acknowledged
+      __syncthreads();
+      if (threadIdx.x == 0) *flag = atomicAdd(rn.cnt + cb, 1) == splits - 1;
+      __syncthreads();
+      if (!*flag) return;
+      // Row rr's 16 float4 of the block are 16 consecutive items, so the
+      // lanes summing a row's squares are 16 aligned lanes of one wave.
+      for (int it = threadIdx.x; it < M * 16; it += blockDim.x) {
+        const int rr = it >> 4, c = n0 + 4 * (it & 15);
+        float sq = 0.f;
+        if (c < N) {
+          const unsigned off = (unsigned)(rr * ncols + c) * 4;
+          float4 t = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(pres, off, 0, kSc1));
+          for (int s0 = 1; s0 < splits; s0 += 8) {
+            float4 u[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              u[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    pres, (unsigned)min(s0 + j, splits - 1) * sstride + off, 0, kSc1));
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              if (s0 + j < splits) {
+                t.x += u[j].x;
+                t.y += u[j].y;
+                t.z += u[j].z;
+                t.w += u[j].w;
+              }
+          }
+          float4* xr = reinterpret_cast<float4*>(epi.x + (size_t)rr * N + c);
+          float4 a = *xr;
+          a.x += t.x * epi.scale;
+          a.y += t.y * epi.scale;
+          a.z += t.z * epi.scale;
+          a.w += t.w * epi.scale;
+          *xr = a;
+          const float4 g = *reinterpret_cast<const float4*>(rn.gain + c);
+          typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+          const f16x4 o = {(_Float16)(a.x * g.x), (_Float16)(a.y * g.y), (_Float16)(a.z * g.z), (_Float16)(a.w * g.w)};
+          *reinterpret_cast<f16x4*>(rn.y + (size_t)rr * N + c) = o;
+          sq = a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+        }
+        sq += __shfl_xor(sq, 8);
+        sq += __shfl_xor(sq, 4);
+        sq += __shfl_xor(sq, 2);
+        sq += __shfl_xor(sq, 1);
+        if ((it & 15) == 0) rn.ss_out[(size_t)rr * ((N + 63) / 64) + cb] = sq;
+      }
+      if (threadIdx.x == 0) __hip_atomic_store(rn.cnt + cb, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+  epi(Cs, LDC, 0, M, n0, 32, 64);
+}
+constexpr int kSkinnyTileBytes = 32 * 68 * 4;
+// LDS row pitch (halfs) of the activation-resident skinny kernel: a K group's
+// largest block count rounded up to 4 blocks (256 bytes), plus 16 bytes.
+__host__ __device__ constexpr int skinny_res_pitch(int steps_per_split, int kw) {
+  return 32 * ((((steps_per_split + kw - 1) / kw) + 3) & ~3) + 8;
+}
+
 template <class Epi, int U, int KW>
 __global__ __launch_bounds__(256 * KW) void k_gemm_skinny(const _Float16* __restrict__ A, int M,
                                                           const _Float16* __restrict__ Wt, int K, int nb,
                                                           int steps_per_split, float* __restrict__ partial, int ncols,
-                                                          Epi epi) {
+                                                          Epi epi, RowNorm rn) {
   constexpr int XP = 32 * U + 8;              // LDS row pitch of an activation chunk (halfs; 16 bytes of padding)
   constexpr int XCH = 32 * (32 * U / 8);      // 16-byte chunks per activation batch (32 rows)
   static_assert(XCH % 256 == 0, "activation chunks split evenly over a group's threads");
   __shared__ __attribute__((aligned(16))) _Float16 xs[KW][2][32 * XP];
+  static_assert(sizeof(xs) >= kSkinnyTileBytes, "the tile fits the activation buffers");
+  __shared__ float rs[32];
+  __shared__ int flag;
+  float ssv[kRowNormLoads];
+  row_norm_loads(ssv, rn, M);
   const int cb = blockIdx.x % nb, split = blockIdx.x / nb;
   const int n0 = cb * 64;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -908,42 +1060,173 @@ __global__ __launch_bounds__(256 * KW) void k_gemm_skinny(const _Float16* __rest
     __syncthreads();
   }
 
-  // acc0[j] of lane l: column 16 rw + 4 (l / 16) + j, row l % 16 (acc1: row
-  // + 16).  K groups add into the tile in group order.
-  constexpr int LDC = 68;
-  static_assert(2 * 32 * XP * 2 >= 32 * LDC * 4, "the tile fits the activation buffers");
-  float* Cs = reinterpret_cast<float*>(&xs[0][0][0]);
   __syncthreads();  // every wave is done with the activations
-  {
-    const int col = 16 * rw + 4 * (lane >> 4), r = lane & 15;
-#pragma unroll
-    for (int g = 0; g < KW; ++g) {
-      if (kg == g) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          Cs[r * LDC + col + j] = (g ? Cs[r * LDC + col + j] : 0.f) + acc0[j];
-          Cs[(r + 16) * LDC + col + j] = (g ? Cs[(r + 16) * LDC + col + j] : 0.f) + acc1[j];
-        }
-      }
-      __syncthreads();
-    }
-  }
-  if (partial) {
-    float* dst = partial + (size_t)split * M * ncols;
-    for (int i = threadIdx.x; i < M * 64; i += blockDim.x) {
-      const int rr = i / 64, c = i % 64;
-      if (n0 + c < ncols) dst[(size_t)rr * ncols + n0 + c] = Cs[rr * LDC + c];
-    }
-    return;
-  }
-  epi(Cs, LDC, 0, M, n0, 32, 64);
+  skinny_tail<Epi, KW>(reinterpret_cast<float*>(&xs[0][0][0]), acc0, acc1, rw, kg, lane, partial, split, gridDim.x / nb,
+                       cb, M, ncols, n0, epi, rn, ssv, rs, &flag);
 }
 
+// Activation-resident variant, for grids of at most two workgroups per CU:
+// every wave issues all of its weight loads at once (at most 32 K blocks, 32
+// KiB per wave), the workgroup's activation range (32 rows x at most 1024 K
+// per K group) goes into LDS once, and each block's MFMAs wait only for that
+// block's weights.  The batched kernel above pays an L2 round trip and a
+// barrier per 256 K of activations, and keeps two batches in flight: at 32
+// rows its gate/up launch took 7.3 us with no weight loads at all.  Loads a
+// wave does not need (blocks past its range, chunks past the group's K) take
+// an offset past the buffer's range, which returns zeros without a memory
+// access, so the issue order stays branch-free.  Wave rw of a K group loads
+// rows rw, rw + 4, ... (16-byte chunks lane + 64 q along the row); the LDS row
+// pitch is 16 bytes past a multiple of 256 bytes, as in the batched kernel,
+// so the B fragment reads stay conflict-free.
+template <class Epi, int NB, int KW>
+__global__ __launch_bounds__(256 * KW) void k_gemm_skinny_res(const _Float16* __restrict__ A, int M,
+                                                              const _Float16* __restrict__ Wt, int K, int nb,
+                                                              int steps_per_split, float* __restrict__ partial,
+                                                              int ncols, Epi epi, RowNorm rn) {
+  constexpr int XQ = (4 * NB + 63) / 64;  // activation chunks per lane and row
+  constexpr unsigned kOob = 0x80000000u;  // past every buffer range here (ranges stay below 2^31 bytes)
+  extern __shared__ __attribute__((aligned(16))) _Float16 xsd[];
+  __shared__ float rs[32];
+  __shared__ int flag;
+  float ssv[kRowNormLoads];
+  row_norm_loads(ssv, rn, M);  // first, so that no later wait covers them
+  const int cb = blockIdx.x % nb, split = blockIdx.x / nb;
+  const int n0 = cb * 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rw = wave & 3, kg = wave >> 2;
+  const int k0 = split * steps_per_split * 32;
+  const int nkb_all = min(K - k0, steps_per_split * 32) / 32;
+  const int kb_lo = (nkb_all * kg) / KW, nkb = (nkb_all * (kg + 1)) / KW - kb_lo;
+  const int kbase = k0 + 32 * kb_lo;
+  const int pitch = skinny_res_pitch(steps_per_split, KW);
+  _Float16* xs = xsd + (size_t)kg * 32 * pitch;
+  // Chunks past the group's K are stored to a 16-byte slot past the tiles.
+  _Float16* sink = xsd + (size_t)KW * 32 * pitch;
+
+  const int nkbt = K / 32;
+  const int rb = 4 * cb + rw;
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)Wt, (short)0, (int)((size_t)((ncols + 15) / 16) * 16 * K * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t xres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((size_t)M * K * 2), 0x00020000);
+  const unsigned wvoff = (unsigned)((((size_t)rb * nkbt + kbase / 32) * 64 + lane) * 16);
+  constexpr int kNt = 2;  // weights are read once per step: streaming policy
+  // Activations first, so that the wait before their LDS stores leaves the
+  // weights in flight.  Rows past M read zeros.
+  f16x8 xv[8][XQ];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int q = 0; q < XQ; ++q) {
+      const int kc = lane + 64 * q;
+      const unsigned off = kc < 4 * nkb ? (unsigned)(((rw + 4 * i) * K + kbase + 8 * kc) * 2) : kOob;
+      xv[i][q] = __builtin_bit_cast(f16x8, __builtin_amdgcn_raw_buffer_load_b128(xres, off, 0, 0));
+    }
+  // The scheduler would otherwise start the LDS stores (and so wait for the
+  // activations) before issuing most of the weight loads.
+  __builtin_amdgcn_sched_barrier(0);
+  // Wave (rb, kg) starts its tiles at block `rot` of its range and wraps
+  // around, so that the waves' first requests do not all fall on 32 KiB
+  // boundaries (every range starts on one).
+  const int rot = nkb > 0 ? (rb * 13 + kg * 7) % nkb : 0;
+  auto blk = [&](int u) { return u + rot < nkb ? u + rot : u + rot - nkb; };
+  f16x8 w[NB];
+#pragma unroll
+  for (int u = 0; u < NB; ++u)
+    w[u] = __builtin_bit_cast(
+        f16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, u < nkb ? wvoff + 1024u * blk(u) : kOob, 0, kNt));
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int q = 0; q < XQ; ++q) {
+      const int kc = lane + 64 * q;
+      _Float16* dst = kc < 4 * nkb ? xs + (rw + 4 * i) * pitch + 8 * kc : sink;
+      *reinterpret_cast<f16x8*>(dst) = xv[i][q];
+    }
+  __syncthreads();
+
+  f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  const _Float16* xb = xs + (lane & 15) * pitch + 8 * (lane >> 4);
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    if (u < nkb) {
+      const int kb = blk(u);
+      const f16x8 b0 = *reinterpret_cast<const f16x8*>(xb + 32 * kb);
+      const f16x8 b1 = *reinterpret_cast<const f16x8*>(xb + 16 * pitch + 32 * kb);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(w[u], b0, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(w[u], b1, acc1, 0, 0, 0);
+    }
+  }
+
+  __syncthreads();  // every wave is done with the activations
+  skinny_tail<Epi, KW>(reinterpret_cast<float*>(xsd), acc0, acc1, rw, kg, lane, partial, split, gridDim.x / nb, cb, M,
+                       ncols, n0, epi, rn, ssv, rs, &flag);
+}
+
+constexpr int kSkinnyResLds = 159 * 1024;  // dynamic LDS limit of the resident kernel
+
+template <class Epi, int NB, int KW>
+static bool skinny_res_go(hipStream_t st, unsigned bytes, const _Float16* A, int M, const _Float16* Wt, int K, int nb,
+                          int splits, int per, float* part, int n_cols, const Epi& e, const RowNorm& rn) {
+  // Once per instantiation, to the largest size the launcher allows (the
+  // kernel's static LDS takes the rest of the 160 KiB).
+  static const hipError_t attr = [] {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_skinny_res<Epi, NB, KW>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, kSkinnyResLds);
+    if (e != hipSuccess) (void)hipGetLastError();  // the batched kernel runs instead
+    return e;
+  }();
+  if (attr != hipSuccess) return false;
+  k_gemm_skinny_res<Epi, NB, KW><<<nb * splits, 256 * KW, bytes, st>>>(A, M, Wt, K, nb, per, part, n_cols, e, rn);
+  return true;
+}
+
+// The activation-resident kernel takes grids of at most two workgroups per CU
+// whose K groups hold at most 32 K blocks (1024 K) each (HH_SKINNY_RES=0 turns
+// it off, for comparison); returns false when the batched kernel is to run.
+template <class Epi>
+static bool launch_skinny_res(hipStream_t st, const _Float16* A, int M, const _Float16* Wt, int K, int nb, int splits,
+                              int per, float* part, int n_cols, int kw, const Epi& e, const RowNorm& rn) {
+  if constexpr (std::is_same<Epi, EpiLogits>::value) {
+    return false;
+  } else {
+    const char* v = getenv("HH_SKINNY_RES");
+    const bool on = !(v && v[0] == '0');
+    const int gmax = (per + kw - 1) / kw;
+    // K-group tiles plus the 16-byte sink for unused chunks.
+    const size_t lds = (size_t)kw * 32 * skinny_res_pitch(per, kw) * 2 + 16;
+    if (!on || (long long)nb * splits > 2 * 256 || gmax > 32 || lds > (size_t)kSkinnyResLds) return false;
+    const unsigned bytes = (unsigned)std::max<size_t>(lds, kSkinnyTileBytes);
+    auto go = [&](auto nbc, auto kwc) {
+      return skinny_res_go<Epi, decltype(nbc)::value, decltype(kwc)::value>(st, bytes, A, M, Wt, K, nb, splits, per,
+                                                                            part, n_cols, e, rn);
+    };
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    if (kw == 2) {
+      if (gmax <= 8) return go(std::integral_constant<int, 8>(), I2());
+      if (gmax <= 16) return go(std::integral_constant<int, 16>(), I2());
+      return go(std::integral_constant<int, 32>(), I2());
+    }
+    if (gmax <= 8) return go(std::integral_constant<int, 8>(), I1());
+    if (gmax <= 16) return go(std::integral_constant<int, 16>(), I1());
+    return go(std::integral_constant<int, 32>(), I1());
+  }
+}
+
+// Returns the K splits, 0 when the shape does not fit the 32-row kernels.
+// rn: see RowNorm; its producer half runs only in the activation-resident
+// kernel of a split residual product (*fused = 1 then, and the partials are
+// consumed in the kernel).
 template <class Epi>
 static int launch_skinny(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, const _Float16* Wt, int K,
-                         int n_cols, const Epi& e, bool defer) {
+                         int n_cols, const Epi& e, bool defer, RowNorm rn, int* fused) {
+  if (fused) *fused = 0;
   // Buffer ranges take 31-bit byte offsets.
   if ((size_t)((n_cols + 15) / 16) * 16 * K * 2 >= ((size_t)1 << 31) || (size_t)32 * K * 2 >= ((size_t)1 << 31)) return 0;
+  // The consumer half reads at most 64 block sums per row.
+  if (rn.ss_in && rn.nss > 4 * kRowNormLoads) return 0;
   const int nb = (n_cols + 63) / 64;
   const int nk = K / 32;
   // Split K only to give about 256 workgroups (at least 8 K blocks each).
@@ -952,16 +1235,37 @@ static int launch_skinny(hipStream_t st, GemmWorkspace ws, const _Float16* A, in
   const int per = (nk + splits - 1) / splits;
   splits = (nk + per - 1) / per;
   float* part = splits > 1 ? ws.ptr : nullptr;
+  if (!(std::is_same<Epi, EpiResid>::value && splits > 1 && n_cols % 64 == 0)) rn.cnt = nullptr;
   // Unsplit (long) K ranges take two K groups per workgroup: eight waves per
   // CU keep more weight loads in flight (gate/up 17.0 -> 15.9 us at 32 rows).
-  if (splits == 1)
-    k_gemm_skinny<Epi, 8, 2><<<nb * splits, 512, 0, st>>>(A, M, Wt, K, nb, per, part, n_cols, e);
-  else
-    k_gemm_skinny<Epi, 8, 1><<<nb * splits, 256, 0, st>>>(A, M, Wt, K, nb, per, part, n_cols, e);
+  const int kw = splits == 1 ? 2 : 1;
+  if (!launch_skinny_res<Epi>(st, A, M, Wt, K, nb, splits, per, part, n_cols, kw, e, rn)) {
+    rn.cnt = nullptr;
+    if (kw == 2)
+      k_gemm_skinny<Epi, 8, 2><<<nb * splits, 512, 0, st>>>(A, M, Wt, K, nb, per, part, n_cols, e, rn);
+    else
+      k_gemm_skinny<Epi, 8, 1><<<nb * splits, 256, 0, st>>>(A, M, Wt, K, nb, per, part, n_cols, e, rn);
+  }
+  if (rn.cnt) {
+    if (fused) *fused = 1;
+    return splits;
+  }
   if (splits > 1 && !defer)
     k_splitk_finalize<Epi><<<((M + kFinRows - 1) / kFinRows) * ((n_cols + 127) / 128), 256, 0, st>>>(
         part, splits, M, n_cols, (n_cols + 127) / 128, e);
   return splits;
+}
+
+// RowNorm consumer fallback for products that no 32-row kernel takes: scale
+// the rows of A (x * gain as fp16) in place by their norm factors.
+__global__ __launch_bounds__(256) void k_rownorm_apply(_Float16* __restrict__ A, int K, RowNorm rn) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  float v = 0.f;
+  if (threadIdx.x == 0)
+    for (int j = 0; j < rn.nss; ++j) v += rn.ss_in[(size_t)row * rn.nss + j];
+  const float inv = rsqrtf(block_sum256(v, red) / rn.n + rn.eps);
+  for (int k = threadIdx.x; k < K; k += 256) A[(size_t)row * K + k] = (_Float16)((float)A[(size_t)row * K + k] * inv);
 }
 
 // Tile choice of a prompt-sized GEMM: {BM, BN, splits}, BM == 0 for the
@@ -1025,17 +1329,25 @@ static int run_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int M, 
 
 // Run C = A W^T over n_cols logical columns with epilogue e; returns the K
 // splits used (with defer, partials of a split run are left in ws.ptr).
+// rn (fp16 operands only): RowNorm's consumer and producer halves, honoured
+// by the 32-row kernels; a consumer request that no 32-row kernel takes
+// scales A's rows first, and *fused says whether the producer half ran.
 template <typename TM, class Epi>
 static int run_gemm(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int n_cols, const Epi& e,
-                    GemmKind kind, bool defer = false, const TM* Wt = nullptr) {
+                    GemmKind kind, bool defer = false, const TM* Wt = nullptr, const RowNorm& rn = RowNorm(),
+                    int* fused = nullptr) {
+  if (fused) *fused = 0;
   if constexpr (sizeof(TM) == 2) {
+    if (M <= 32 && Wt && K % 64 == 0) {
+      const int sp = launch_skinny(st, ws, reinterpret_cast<const _Float16*>(A), M,
+                                   reinterpret_cast<const _Float16*>(Wt), K, n_cols, e, defer, rn, fused);
+      if (sp > 0) return sp;
+    }
+    if (rn.ss_in)
+      k_rownorm_apply<<<M, 256, 0, st>>>(reinterpret_cast<_Float16*>(const_cast<TM*>(A)), K, rn);
     if (K % 64 == 0) {
       const _Float16* Ah = reinterpret_cast<const _Float16*>(A);
       const _Float16* Wh = reinterpret_cast<const _Float16*>(W);
-      if (M <= 32 && Wt) {
-        const int sp = launch_skinny(st, ws, Ah, M, reinterpret_cast<const _Float16*>(Wt), K, n_cols, e, defer);
-        if (sp > 0) return sp;
-      }
       if constexpr (!std::is_same<Epi, EpiLogits>::value) {
         const int sp = run_wide(st, ws, Ah, M, Wh, K, n_cols, e, kind, defer);
         if (sp > 0) return sp;
@@ -1139,9 +1451,9 @@ template <typename TM, typename TKV>
 int GemmKernels<TM, TKV>::qkv_deferred(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int hq,
                                        int hkv, float scale, const int* row_stream, const int* row_pos,
                                        const float2* rope, float* q, TKV* kv, KvLayout L, int layer,
-                                       const int* page_table, const TM* Wt) {
+                                       const int* page_table, const TM* Wt, const RowNorm& rn) {
   EpiQKV<TKV> e{hq, hkv, scale, row_stream, row_pos, rope, q, nullptr, kv, L, layer, page_table};
-  return run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e, GemmKind::QKV, true, Wt);
+  return run_gemm<TM>(st, ws, A, M, W, d, (hq + 2 * hkv) * 64, e, GemmKind::QKV, true, Wt, rn);
 }
 
 template <typename TM, typename TKV>
@@ -1150,12 +1462,24 @@ bool GemmKernels<TM, TKV>::norm_fusable(int N) {
 }
 
 template <typename TM, typename TKV>
-void GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale,
-                                 float* x, const float* gain, float eps, TM* h, const TM* Wt) {
+bool GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N,
+                                 float scale, float* x, const float* gain, float eps, TM* h, const TM* Wt, float* ss,
+                                 int* cnt) {
   EpiResid e{N, scale, x};
   const bool norm = gain != nullptr;
-  const int sp = run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid, norm, Wt);
-  if (norm) k_resid_norm<TM><<<M, 256, 0, st>>>(ws.ptr, sp > 1 ? sp : 0, M, N, scale, x, gain, eps, h);
+  RowNorm rn;
+  if constexpr (sizeof(TM) == 2) {
+    if (norm && ss && cnt) {
+      rn.cnt = cnt;
+      rn.gain = gain;
+      rn.y = reinterpret_cast<_Float16*>(h);
+      rn.ss_out = ss;
+    }
+  }
+  int fused = 0;
+  const int sp = run_gemm<TM>(st, ws, A, M, W, K, N, e, GemmKind::Resid, norm, Wt, rn, &fused);
+  if (norm && !fused) k_resid_norm<TM><<<M, 256, 0, st>>>(ws.ptr, sp > 1 ? sp : 0, M, N, scale, x, gain, eps, h);
+  return fused != 0;
 }
 
 template <typename TM, typename TKV>
@@ -1165,17 +1489,18 @@ void GemmKernels<TM, TKV>::rmsnorm(hipStream_t st, int M, float* x, int N, const
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::gateup(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int F, float scale,
-                                  TM* m, const TM* Wt) {
+                                  TM* m, const TM* Wt, const RowNorm& rn) {
   // Groups of 32 gate + 32 up columns: every tile width here is a multiple of 64.
   EpiGateUp<TM> e{F, 32, scale, m};
-  run_gemm<TM>(st, ws, A, M, W, d, ((F + 31) / 32) * 64, e, GemmKind::GateUp, false, Wt);
+  run_gemm<TM>(st, ws, A, M, W, d, ((F + 31) / 32) * 64, e, GemmKind::GateUp, false, Wt, rn);
 }
 
 template <typename TM, typename TKV>
 void GemmKernels<TM, TKV>::logits(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int d, int V, float scale,
-                                  float* logits, unsigned long long* slot, const int* row_stream, const TM* Wt) {
+                                  float* logits, unsigned long long* slot, const int* row_stream, const TM* Wt,
+                                  const RowNorm& rn) {
   EpiLogits e{V, scale, logits, slot, row_stream};
-  run_gemm<TM>(st, ws, A, M, W, d, V, e, GemmKind::Logits, false, Wt);
+  run_gemm<TM>(st, ws, A, M, W, d, V, e, GemmKind::Logits, false, Wt, rn);
 }
 
 template struct GemmKernels<float, float>;

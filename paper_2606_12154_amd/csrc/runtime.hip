@@ -47,6 +47,9 @@ struct Layout {
   size_t lm_headQ;
   size_t final_norm, rope, kv, page_table, pos, pending, slot, hist, ll, ll_words, layer_tab, trace;
   size_t row_stream, row_pos, feed, x, h, q, qM, o32, oM, m32, mM, part, logits, gemm_ws, gemm_ws_bytes, scratch_u32;
+  // RowNorm buffers of the lockstep decode rows: column-block counters (zero
+  // between launches; in the zero-initialised range) and row sums of squares.
+  size_t nrm_cnt, nrm_ss;
   size_t total;
 };
 
@@ -181,6 +184,7 @@ Layout make_layout(const hh_config& c) {
   L.ll = take(L.ll_words * 8);
   L.layer_tab = take((size_t)c.n_layers * sizeof(LayerPtrs<float>));
   L.trace = take((size_t)kMaxStepWG * (c.n_layers + 1) * 32 * 8);  // optional phase timestamps
+  L.nrm_cnt = take((size_t)(16384 / 64) * 4);
   const size_t R = L.rows_cap, tm = bf ? 2 : 4;
   L.row_stream = take(R * 4);
   L.row_pos = take(R * 4);
@@ -199,6 +203,7 @@ Layout make_layout(const hh_config& c) {
   L.gemm_ws_bytes = std::min<size_t>((size_t)4 * R * std::max((size_t)2 * F, (size_t)L.nqkv) * 4, (size_t)256 << 20);
   L.gemm_ws = take(L.gemm_ws_bytes);
   L.scratch_u32 = take(256);
+  L.nrm_ss = take((size_t)32 * (16384 / 64) * 4);
   L.total = off;
   return L;
 }
@@ -292,6 +297,20 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
   const int* pt = c->at<int>(L.page_table);
   const float2* rope = c->at<float2>(L.rope);
   unsigned long long* slot = c->at<unsigned long long>(L.slot);
+  // Lockstep decode rows on fp16 operands with tiled weights split each
+  // RMSNorm across the residual product that feeds it and the product that
+  // reads it (RowNorm); `pending`: h holds x * gain and the row sums of
+  // squares are in nrm_ss, not yet applied.
+  const bool rnorm = sizeof(TM) == 2 && !decode_gemv && prefill_stream < 0 && head_row == -1 &&
+                     !L.wqkvT16.empty() && GK::norm_fusable(d) && d / 64 <= 64;
+  float* nss = rnorm ? c->at<float>(L.nrm_ss) : nullptr;
+  int* ncnt = rnorm ? c->at<int>(L.nrm_cnt) : nullptr;
+  RowNorm rn_use;
+  rn_use.ss_in = nss;
+  rn_use.nss = d / 64;
+  rn_use.n = (float)d;
+  rn_use.eps = eps;
+  bool pending = false;
   for (int l = 0; l < g.n_layers; ++l) {
     const float* an = c->at<float>(L.attn_norm[l]);
     const float* mn = c->at<float>(L.mlp_norm[l]);
@@ -322,7 +341,8 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       QkvFold<TKV> qf;
       if (fold) {
         const int sp = GK::qkv_deferred(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, q, kv, kl, l,
-                                        pt, tiled ? c->at<TM>(L.wqkvT16[l]) : nullptr);
+                                        pt, tiled ? c->at<TM>(L.wqkvT16[l]) : nullptr,
+                                        pending ? rn_use : RowNorm());
         if (sp > 1) qf = QkvFold<TKV>{gws.ptr, sp, (hq + 2 * hkv) * 64, ws, rope, kv};
       } else {
         GK::qkv(st, gws, h, n, c->at<TM>(L.wqkvM[l]), d, hq, hkv, ws, rs, rp, rope, flash ? nullptr : q,
@@ -339,15 +359,18 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       }
       const TM* wo_t = tiled ? c->at<TM>(L.woT16[l]) : nullptr;
       if (fuse) {
-        GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h, wo_t);
+        pending = GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h, wo_t, nss, ncnt);
       } else {
         GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, nullptr, 0.f, nullptr, wo_t);
         DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
       }
-      GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM, tiled ? c->at<TM>(L.wguT16[l]) : nullptr);
+      GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM, tiled ? c->at<TM>(L.wguT16[l]) : nullptr,
+                 pending ? rn_use : RowNorm());
+      // The final norm stays a pass of its own: the head's thousands of
+      // workgroups would each recompute the row factors.
       const float* next_an = (fuse && l + 1 < g.n_layers) ? c->at<float>(L.attn_norm[l + 1]) : nullptr;
-      GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h,
-                tiled ? c->at<TM>(L.wdownT16[l]) : nullptr);
+      pending = GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h,
+                          tiled ? c->at<TM>(L.wdownT16[l]) : nullptr, next_an ? nss : nullptr, ncnt);
     }
   }
   const float* fn = c->at<float>(L.final_norm);

@@ -113,8 +113,7 @@ def test_decode_teacher_forced(one_b, ctx):
     print(f"1B teacher-forced decode: max-abs {worst:.4g}")
 
 
-def test_multistream_lockstep(one_b, ctx):
-    shape, _, model = one_b
+def multistream_lockstep(model, shape, ctx, what):
     lens = [16, 33, 7, 48]
     prompts = [synth.make_tokens(shape.vocab, n, 100 + i) for i, n in enumerate(lens)]
     ctx.reset()
@@ -128,8 +127,38 @@ def test_multistream_lockstep(one_b, ctx):
         feed = rng.integers(0, shape.vocab, size=4).astype(np.int32)
         _, lg = ctx.decode_step([0, 1, 2, 3], feed, logits=True)
         ref = model.decode_batch(caches, feed)
-        worst = max(worst, check_logits(lg, ref, TOL, what=f"multi step {step}"))
-    print(f"1B 4-stream decode: max-abs {worst:.4g}")
+        worst = max(worst, check_logits(lg, ref, TOL, what=f"{what} step {step}"))
+    print(f"{what}: max-abs {worst:.4g}")
+
+
+def test_multistream_lockstep(one_b, ctx):
+    """Four ragged streams in lockstep (prompts of up to 48 tokens run through
+    the skinny GEMMs too), activation-resident skinny kernel."""
+    shape, _, model = one_b
+    multistream_lockstep(model, shape, ctx, "1B 4-stream decode")
+
+
+def test_multistream_lockstep_batched_skinny(one_b):
+    """The same with the batched skinny kernel (HH_SKINNY_RES=0), which
+    serves grids or K ranges the resident one does not take; a context of its
+    own, run eagerly, so that no graph captured under the default is
+    replayed."""
+    shape, tensors, model = one_b
+    saved = {k: os.environ.get(k) for k in ("HH_SKINNY_RES", "HH_GRAPHS")}
+    os.environ["HH_SKINNY_RES"] = "0"
+    os.environ["HH_GRAPHS"] = "0"
+    c = None
+    try:
+        c = new_context(shape, tensors, streams=5, context=512, max_prefill=256)
+        multistream_lockstep(model, shape, c, "1B 4-stream decode, batched skinny kernel")
+    finally:
+        if c is not None:
+            c.close()
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
 
 
 @pytest.fixture(scope="module")
