@@ -458,8 +458,10 @@ __global__ __launch_bounds__(64) void k_attn_combine(const float* __restrict__ p
 // Paged GQA attention for decode rows: one 512-thread workgroup per (row,
 // kv head) serves the G query heads of that kv head, so each K/V page is
 // read once.  The row's page list is staged in LDS; wave w takes pages w,
-// w + 8, ... with the next two pages' K/V in flight in two more register
-// sets (strict rotation, no register copies).  Lane (key = lane / 4, quarter =
+// w + 8, ..., its first four (three for fp32 caches or eight query heads)
+// all issued at the start, later ones with the next two pages' K/V in flight
+// in two more register sets (strict rotation, no register copies).  Lane
+// (key = lane / 4, quarter =
 // lane % 4) holds 16 dims of one key; scores use exp2 with 1/sqrt(64)*log2(e)
 // folded into q; each head keeps its own online softmax state.  The waves'
 // states are merged in LDS, one wave per head.
@@ -499,24 +501,58 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
   __shared__ float qkv_s[(G + 2) * 64];
   __shared__ TKV new_kv[2][64];
   const int g = blockIdx.x, r = blockIdx.y;
+  const bool folded = fold.part != nullptr;
+  const int hkv = hq / G;
+  // Folded QKV: column c < (G + 2) 64 of this row's slice (q heads, then k,
+  // then v of head g); thread t takes columns t + NT i.
+  constexpr int CPT = ((G + 2) * 64 + NT - 1) / NT;
+  auto fold_col = [&](int c) {
+    return c < G * 64 ? g * G * 64 + c
+                      : (c < (G + 1) * 64 ? (hq + g) * 64 + (c - G * 64) : (hq + hkv + g) * 64 + (c - (G + 1) * 64));
+  };
+  // The first eight split partials of those columns load before anything
+  // else: they depend on nothing, and the row's position and page list are
+  // two dependent round trips away.  Clamped indices; extras unused.
+  float fp[CPT][8];
+  if (folded) {
+    const size_t stride = (size_t)gridDim.y * fold.ncols;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = min(threadIdx.x + NT * i, (G + 2) * 64 - 1);
+      const float* pp = fold.part + (size_t)r * fold.ncols + fold_col(c);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) fp[i][j] = pp[min(j, fold.splits - 1) * stride];
+    }
+  }
   const int s = row_stream[r], p = row_pos[r], t = p + 1, npg = (t + kPage - 1) / kPage;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, key = lane >> 2, quarter = lane & 3;
   const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
-  for (int i = threadIdx.x; i < npg && i < kRowsMaxPages; i += NT) pts[i] = page_table[(size_t)s * L.max_pages + i];
-  auto page_of = [&](int pg) { return pg < kRowsMaxPages ? pts[pg] : page_table[(size_t)s * L.max_pages + pg]; };
-  const bool folded = fold.part != nullptr;
-  // Pages wave, wave + 8, ...: the next two pages' K/V are in flight while
-  // one is taken (three register sets in rotation); loads past the end
-  // re-read the row's last page.  The first two are issued before the folded
-  // QKV reduction, whose loads they overlap (the row's own key, which the
-  // reduction writes, is taken from LDS, not from these loads).
-  KvPage<TKV> A, B, C;
-  if (!folded) __syncthreads();  // pts
-  if (wave < npg) {
-    kv_page_load(A, kv, L, layer, folded ? page_table[(size_t)s * L.max_pages + wave] : page_of(wave), g, key, quarter);
-    const int pg1 = min(wave + NW, npg - 1);
-    kv_page_load(B, kv, L, layer, folded ? page_table[(size_t)s * L.max_pages + pg1] : page_of(pg1), g, key, quarter);
-  }
+  // Rotation of the pair (e, e + 32) this thread applies below (q heads and k).
+  float2 cs = make_float2(1.f, 0.f);
+  if (folded && threadIdx.x < (G + 1) * 32) cs = fold.rope[(size_t)p * 32 + (threadIdx.x & 31)];
+  // Pages wave, wave + 8, ...: the wave's first PU pages are all issued here,
+  // before the folded QKV reduction, whose loads they overlap (the row's own
+  // key, which the reduction writes, is taken from LDS, not from these
+  // loads); their page ids (and the new key's page) come straight from the
+  // table, one round trip after the row's position.  Waves with fewer pages
+  // re-read the row's last page, so that every wave issues the same loads
+  // and the waits stay exact (spreading those re-reads over the row's pages
+  // measured the same).  The LDS copy of the page list serves rows
+  // longer than PU * 8 pages, which continue below with three register sets
+  // in rotation.
+  constexpr int PU = sizeof(TKV) == 2 && G <= 4 ? 4 : 3;
+  const int* prow = page_table + (size_t)s * L.max_pages;
+  int pid[PU];
+#pragma unroll
+  for (int k = 0; k < PU; ++k) pid[k] = prow[min(wave + NW * k, npg - 1)];
+  const int new_page = folded ? prow[p / kPage] : 0;
+  const bool long_row = npg > PU * NW;
+  if (long_row)
+    for (int i = threadIdx.x; i < npg && i < kRowsMaxPages; i += NT) pts[i] = prow[i];
+  auto page_of = [&](int pg) { return pg < kRowsMaxPages ? pts[pg] : prow[pg]; };
+  KvPage<TKV> P[PU];
+#pragma unroll
+  for (int k = 0; k < PU; ++k) kv_page_load(P[k], kv, L, layer, pid[k], g, key, quarter);
   float qv[G][16];
   if (!folded) {
 #pragma unroll
@@ -526,23 +562,27 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
   } else {
     // Sum the split partials of the row's columns in split order and scale
     // them (the reduction the QKV epilogue would otherwise run).
-    const int hkv = hq / G;
     const size_t stride = (size_t)gridDim.y * fold.ncols;
-    for (int c = threadIdx.x; c < (G + 2) * 64; c += NT) {
-      const int col = c < G * 64 ? g * G * 64 + c
-                                 : (c < (G + 1) * 64 ? (hq + g) * 64 + (c - G * 64) : (hq + hkv + g) * 64 + (c - (G + 1) * 64));
-      const float* pp = fold.part + (size_t)r * fold.ncols + col;
-      float v = 0.f;
-      // Eight partials in flight at a time (clamped indices, extras unused).
-      for (int s0 = 0; s0 < fold.splits; s0 += 8) {
-        float u[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) u[j] = pp[min(s0 + j, fold.splits - 1) * stride];
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + NT * i;
+      if (c < (G + 2) * 64) {
+        float v = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          if (s0 + j < fold.splits) v += u[j];
+          if (j < fold.splits) v += fp[i][j];
+        // More than eight splits: the rest eight at a time.
+        const float* pp = fold.part + (size_t)r * fold.ncols + fold_col(c);
+        for (int s0 = 8; s0 < fold.splits; s0 += 8) {
+          float u[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) u[j] = pp[min(s0 + j, fold.splits - 1) * stride];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (s0 + j < fold.splits) v += u[j];
+        }
+        qkv_s[c] = v * fold.scale;
       }
-      qkv_s[c] = v * fold.scale;
     }
     __syncthreads();  // pts, qkv_s
 
@@ -552,8 +592,8 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       const int hh = i >> 5, e = i & 31;
       float y0 = qkv_s[hh * 64 + e], y1 = qkv_s[hh * 64 + e + 32];
       if (hh <= G) {
-        const float2 cs = fold.rope[(size_t)p * 32 + e];
-        const float r0 = y0 * cs.x - y1 * cs.y, r1 = y1 * cs.x + y0 * cs.y;
+        const float2 c2 = i == (int)threadIdx.x ? cs : fold.rope[(size_t)p * 32 + e];
+        const float r0 = y0 * c2.x - y1 * c2.y, r1 = y1 * c2.x + y0 * c2.y;
         y0 = r0;
         y1 = r1;
       }
@@ -565,7 +605,7 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
         const TKV a = (TKV)y0, b = (TKV)y1;
         new_kv[kind][e] = a;
         new_kv[kind][e + 32] = b;
-        TKV* dst = fold.kv + L.head_tile(layer, page_of(p / kPage), kind, g) + (p % kPage) * 64;
+        TKV* dst = fold.kv + L.head_tile(layer, new_page, kind, g) + (p % kPage) * 64;
         dst[e] = a;
         dst[e + 32] = b;
       }
@@ -627,8 +667,18 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       m[h] = mn;
     }
   };
-  if (wave < npg) {
-    for (int pg = wave; pg < npg; pg += 3 * NW) {
+#pragma unroll
+  for (int k = 0; k < PU; ++k)
+    if (wave + NW * k < npg) take(P[k], wave + NW * k);
+  // Longer rows: the next two pages' K/V are in flight while one is taken;
+  // loads past the end re-read the row's last page.
+  if (long_row) __syncthreads();  // pts (the folded path's barriers came earlier)
+  if (wave + NW * PU < npg) {
+    KvPage<TKV>&A = P[0], &B = P[1], &C = P[2];
+    const int pg0 = wave + NW * PU;
+    kv_page_load(A, kv, L, layer, page_of(pg0), g, key, quarter);
+    kv_page_load(B, kv, L, layer, page_of(min(pg0 + NW, npg - 1)), g, key, quarter);
+    for (int pg = pg0; pg < npg; pg += 3 * NW) {
       kv_page_load(C, kv, L, layer, page_of(min(pg + 2 * NW, npg - 1)), g, key, quarter);
       take(A, pg);
       if (pg + NW >= npg) break;

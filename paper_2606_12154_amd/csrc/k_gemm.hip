@@ -887,6 +887,19 @@ __device__ __forceinline__ void skinny_tail(float* Cs, const f32x4& acc0, const 
       const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
           (void*)partial, (short)0, (int)((size_t)splits * M * ncols * 4), 0x00020000);
       const unsigned sstride = (unsigned)M * ncols * 4;  // bytes of one split's partials
+      // Items: row rr = it / 16, four columns n0 + 4 (it % 16); a row's 16
+      // items are 16 aligned lanes of one wave (M * 16 <= 512 <= 2 blockDim).
+      // Every split loads its items' x and gains before counting itself in,
+      // so the last one does not wait for them afterwards.
+      float4 xa[2], ga[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int it = threadIdx.x + blockDim.x * k, rr = it >> 4, c = n0 + 4 * (it & 15);
+        if (it < M * 16 && c < N) {
+          xa[k] = *reinterpret_cast<const float4*>(epi.x + (size_t)rr * N + c);
+          ga[k] = *reinterpret_cast<const float4*>(rn.gain + c);
+        }
+      }
       for (int it = threadIdx.x; it < M * 16; it += blockDim.x) {
         const int rr = it >> 4, c = n0 + 4 * (it & 15);
         if (c < ncols) {
@@ -900,37 +913,48 @@ __device__ __forceinline__ void skinny_tail(float* Cs, const f32x4& acc0, const 
       if (threadIdx.x == 0) *flag = atomicAdd(rn.cnt + cb, 1) == splits - 1;
       __syncthreads();
       if (!*flag) return;
-      // Row rr's 16 float4 of the block are 16 consecutive items, so the
-      // lanes summing a row's squares are 16 aligned lanes of one wave.
-      for (int it = threadIdx.x; it < M * 16; it += blockDim.x) {
-        const int rr = it >> 4, c = n0 + 4 * (it & 15);
+      // Up to 8 splits: both items' partials are loaded at once; more splits
+      // go 8 at a time.  Either way they are summed in split order.
+      float4 t[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) t[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int s0 = 0; s0 < splits; s0 += 8) {
+        float4 u[2][8];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int it = threadIdx.x + blockDim.x * k, rr = it >> 4, c = n0 + 4 * (it & 15);
+          const bool ok = it < M * 16 && c < N;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            u[k][j] = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(
+                            pres, ok && s0 + j < splits ? (unsigned)(s0 + j) * sstride + (unsigned)(rr * ncols + c) * 4
+                                                        : 0x80000000u,
+                            0, kSc1));
+        }
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (s0 + j < splits) {
+              t[k].x += u[k][j].x;
+              t[k].y += u[k][j].y;
+              t[k].z += u[k][j].z;
+              t[k].w += u[k][j].w;
+            }
+      }
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int it = threadIdx.x + blockDim.x * k, rr = it >> 4, c = n0 + 4 * (it & 15);
         float sq = 0.f;
-        if (c < N) {
-          const unsigned off = (unsigned)(rr * ncols + c) * 4;
-          float4 t = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(pres, off, 0, kSc1));
-          for (int s0 = 1; s0 < splits; s0 += 8) {
-            float4 u[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-              u[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                    pres, (unsigned)min(s0 + j, splits - 1) * sstride + off, 0, kSc1));
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-              if (s0 + j < splits) {
-                t.x += u[j].x;
-                t.y += u[j].y;
-                t.z += u[j].z;
-                t.w += u[j].w;
-              }
-          }
-          float4* xr = reinterpret_cast<float4*>(epi.x + (size_t)rr * N + c);
-          float4 a = *xr;
-          a.x += t.x * epi.scale;
-          a.y += t.y * epi.scale;
-          a.z += t.z * epi.scale;
-          a.w += t.w * epi.scale;
-          *xr = a;
-          const float4 g = *reinterpret_cast<const float4*>(rn.gain + c);
+        if (it < M * 16 && c < N) {
+          float4 a = xa[k];
+          a.x += t[k].x * epi.scale;
+          a.y += t[k].y * epi.scale;
+          a.z += t[k].z * epi.scale;
+          a.w += t[k].w * epi.scale;
+          *reinterpret_cast<float4*>(epi.x + (size_t)rr * N + c) = a;
+          const float4 g = ga[k];
           typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
           const f16x4 o = {(_Float16)(a.x * g.x), (_Float16)(a.y * g.y), (_Float16)(a.z * g.z), (_Float16)(a.w * g.w)};
           *reinterpret_cast<f16x4*>(rn.y + (size_t)rr * N + c) = o;
@@ -940,7 +964,7 @@ __device__ __forceinline__ void skinny_tail(float* Cs, const f32x4& acc0, const 
         sq += __shfl_xor(sq, 4);
         sq += __shfl_xor(sq, 2);
         sq += __shfl_xor(sq, 1);
-        if ((it & 15) == 0) rn.ss_out[(size_t)rr * ((N + 63) / 64) + cb] = sq;
+        if (it < M * 16 && (it & 15) == 0) rn.ss_out[(size_t)rr * ((N + 63) / 64) + cb] = sq;
       }
       if (threadIdx.x == 0) __hip_atomic_store(rn.cnt + cb, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
