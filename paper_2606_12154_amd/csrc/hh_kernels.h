@@ -64,15 +64,17 @@ struct GemmWorkspace {
 //    64-column block to finish adds the split sum (in split order) into x,
 //    writes y = x * gain (elementwise) as fp16 and the block's per-row sums
 //    of squares to ss_out[row * (N / 64) + block]; cnt holds one counter per
-//    column block, zero before and after every launch;
-//  * consumer: row r of A is such a y; the product's row r is scaled by
-//    rsqrt(sum over blocks of ss_in[r * nss + j] / n + eps) before its
-//    split partials or epilogue.
+//    column block (ncnt of them), zero before and after every launch;
+//  * consumer: row r of A is such a y (nss <= 32 block sums per row, a
+//    multiple of 4); the product's row r is scaled by rsqrt(sum over blocks
+//    of ss_in[r * nss + j] / n + eps) before its split partials or
+//    epilogue.
 struct RowNorm {
   const float* ss_in = nullptr;
   int nss = 0;
   float n = 1.f, eps = 0.f;
   int* cnt = nullptr;
+  int ncnt = 0;
   const float* gain = nullptr;
   _Float16* y = nullptr;
   float* ss_out = nullptr;
@@ -94,12 +96,13 @@ struct GemmKernels {
                           const RowNorm& rn = RowNorm());
   // x += A W^T * scale; with gain, then h = rmsnorm(x) * gain (fused into the
   // split-K reduction when K is split).  Requires norm_fusable(N) with gain.
-  // With ss and cnt (RowNorm's producer buffers) the 32-row GEMM may instead
-  // leave h = x * gain and the row sums of squares in ss: returns true then,
-  // and the product reading h takes RowNorm{ss, N / 64, N, eps}.
+  // With ss and cnt (RowNorm's producer buffers, ncnt counters) the 32-row
+  // GEMM may instead leave h = x * gain and the row sums of squares in ss:
+  // returns true then, and the product reading h takes
+  // RowNorm{ss, N / 64, N, eps}.
   static bool resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N, float scale, float* x,
                     const float* gain = nullptr, float eps = 0.f, TM* h = nullptr, const TM* Wt = nullptr,
-                    float* ss = nullptr, int* cnt = nullptr);
+                    float* ss = nullptr, int* cnt = nullptr, int ncnt = 0);
   static bool norm_fusable(int N);
   // h = rmsnorm(x) * gain, one row per workgroup (norm_fusable(N)).
   static void rmsnorm(hipStream_t st, int M, float* x, int N, const float* gain, float eps, TM* h);

@@ -808,22 +808,18 @@ static int launch_wide(hipStream_t st, GemmWorkspace ws, const _Float16* A, int 
 // B fragment reads conflict-free).  The finished 64-column tile goes through
 // LDS into the usual epilogue, or into split partials when K is split to give
 // every CU work.
-// RowNorm consumer: threads 0..127 each load 16 of a row's block sums of
-// squares (row t / 4, blocks t % 4 + 4 i; zeros past M rows or nss blocks,
-// so nss <= 64) early, so that the tail finds them landed.
-constexpr int kRowNormLoads = 16;
-__device__ __forceinline__ void row_norm_loads(float (&ssv)[kRowNormLoads], const RowNorm& rn, int M) {
-  if (!rn.ss_in || threadIdx.x >= 128) return;
+// RowNorm consumer of the 32-row kernels: thread t < 256 loads float4 t % 8
+// of row t / 8's block sums (nss <= 32, a multiple of 4; eight consecutive
+// lanes read one row's 128 bytes) first thing, so that the tail finds them
+// landed (zeros past M rows or nss sums).
+__device__ __forceinline__ void row_norm_loads(float4& ssv, const RowNorm& rn, int M) {
+  if (!rn.ss_in || threadIdx.x >= 256) return;
   const __amdgpu_buffer_rsrc_t res =
       __builtin_amdgcn_make_buffer_rsrc((void*)rn.ss_in, (short)0, (int)((size_t)M * rn.nss * 4), 0x00020000);
-  const int r = threadIdx.x >> 2, part = threadIdx.x & 3;
-#pragma unroll
-  for (int i = 0; i < kRowNormLoads; ++i) {
-    const int j = part + 4 * i;
-    ssv[i] = __builtin_bit_cast(
-        float, __builtin_amdgcn_raw_buffer_load_b32(res, j < rn.nss && r < M ? (unsigned)((r * rn.nss + j) * 4) : 0x80000000u,
-                                                    0, 0));
-  }
+  const int r = threadIdx.x >> 3, q = threadIdx.x & 7;
+  ssv = __builtin_bit_cast(
+      float4, __builtin_amdgcn_raw_buffer_load_b128(
+                  res, r < M && 4 * q < rn.nss ? (unsigned)((r * rn.nss + 4 * q) * 4) : 0x80000000u, 0, 0));
 }
 
 // acc0[j] of lane l: column 16 rw + 4 (l / 16) + j, row l % 16 (acc1: row
@@ -837,18 +833,17 @@ template <class Epi, int KW>
 __device__ __forceinline__ void skinny_tail(float* Cs, const f32x4& acc0, const f32x4& acc1, int rw, int kg, int lane,
                                             float* __restrict__ partial, int split, int splits, int cb, int M,
                                             int ncols, int n0, const Epi& epi, const RowNorm& rn,
-                                            const float (&ssv)[kRowNormLoads], float* rs, int* flag) {
+                                            const float4& ssv, float* rs, int* flag) {
   constexpr int LDC = 68;
   const int col = 16 * rw + 4 * (lane >> 4), r = lane & 15;
   float f0 = 1.f, f1 = 1.f;  // norm factors of rows r and r + 16
   if (rn.ss_in) {
-    if (threadIdx.x < 128) {
-      float v = 0.f;
-#pragma unroll
-      for (int i = 0; i < kRowNormLoads; ++i) v += ssv[i];
+    if (threadIdx.x < 256) {
+      float v = (ssv.x + ssv.y) + (ssv.z + ssv.w);
       v += __shfl_xor(v, 1);
       v += __shfl_xor(v, 2);
-      if ((threadIdx.x & 3) == 0) rs[threadIdx.x >> 2] = rsqrtf(v / rn.n + rn.eps);
+      v += __shfl_xor(v, 4);
+      if ((threadIdx.x & 7) == 0) rs[threadIdx.x >> 3] = rsqrtf(v / rn.n + rn.eps);
     }
     __syncthreads();
     f0 = rs[r];
@@ -991,7 +986,7 @@ __global__ __launch_bounds__(256 * KW) void k_gemm_skinny(const _Float16* __rest
   static_assert(sizeof(xs) >= kSkinnyTileBytes, "the tile fits the activation buffers");
   __shared__ float rs[32];
   __shared__ int flag;
-  float ssv[kRowNormLoads];
+  float4 ssv = make_float4(0.f, 0.f, 0.f, 0.f);
   row_norm_loads(ssv, rn, M);
   const int cb = blockIdx.x % nb, split = blockIdx.x / nb;
   const int n0 = cb * 64;
@@ -1112,7 +1107,7 @@ __global__ __launch_bounds__(256 * KW) void k_gemm_skinny_res(const _Float16* __
   extern __shared__ __attribute__((aligned(16))) _Float16 xsd[];
   __shared__ float rs[32];
   __shared__ int flag;
-  float ssv[kRowNormLoads];
+  float4 ssv = make_float4(0.f, 0.f, 0.f, 0.f);
   row_norm_loads(ssv, rn, M);  // first, so that no later wait covers them
   const int cb = blockIdx.x % nb, split = blockIdx.x / nb;
   const int n0 = cb * 64;
@@ -1249,8 +1244,8 @@ static int launch_skinny(hipStream_t st, GemmWorkspace ws, const _Float16* A, in
   if (fused) *fused = 0;
   // Buffer ranges take 31-bit byte offsets.
   if ((size_t)((n_cols + 15) / 16) * 16 * K * 2 >= ((size_t)1 << 31) || (size_t)32 * K * 2 >= ((size_t)1 << 31)) return 0;
-  // The consumer half reads at most 64 block sums per row.
-  if (rn.ss_in && rn.nss > 4 * kRowNormLoads) return 0;
+  // The consumer half reads at most 32 block sums per row (a multiple of 4).
+  if (rn.ss_in && (rn.nss > 32 || rn.nss % 4)) return 0;
   const int nb = (n_cols + 63) / 64;
   const int nk = K / 32;
   // Split K only to give about 256 workgroups (at least 8 K blocks each).
@@ -1259,7 +1254,7 @@ static int launch_skinny(hipStream_t st, GemmWorkspace ws, const _Float16* A, in
   const int per = (nk + splits - 1) / splits;
   splits = (nk + per - 1) / per;
   float* part = splits > 1 ? ws.ptr : nullptr;
-  if (!(std::is_same<Epi, EpiResid>::value && splits > 1 && n_cols % 64 == 0)) rn.cnt = nullptr;
+  if (!(std::is_same<Epi, EpiResid>::value && splits > 1 && n_cols % 64 == 0 && nb <= rn.ncnt)) rn.cnt = nullptr;
   // Unsplit (long) K ranges take two K groups per workgroup: eight waves per
   // CU keep more weight loads in flight (gate/up 17.0 -> 15.9 us at 32 rows).
   const int kw = splits == 1 ? 2 : 1;
@@ -1488,13 +1483,14 @@ bool GemmKernels<TM, TKV>::norm_fusable(int N) {
 template <typename TM, typename TKV>
 bool GemmKernels<TM, TKV>::resid(hipStream_t st, GemmWorkspace ws, const TM* A, int M, const TM* W, int K, int N,
                                  float scale, float* x, const float* gain, float eps, TM* h, const TM* Wt, float* ss,
-                                 int* cnt) {
+                                 int* cnt, int ncnt) {
   EpiResid e{N, scale, x};
   const bool norm = gain != nullptr;
   RowNorm rn;
   if constexpr (sizeof(TM) == 2) {
     if (norm && ss && cnt) {
       rn.cnt = cnt;
+      rn.ncnt = ncnt;
       rn.gain = gain;
       rn.y = reinterpret_cast<_Float16*>(h);
       rn.ss_out = ss;

@@ -50,6 +50,7 @@ struct Layout {
   // RowNorm buffers of the lockstep decode rows: column-block counters (zero
   // between launches; in the zero-initialised range) and row sums of squares.
   size_t nrm_cnt, nrm_ss;
+  int nrm_ncnt;
   size_t total;
 };
 
@@ -184,7 +185,9 @@ Layout make_layout(const hh_config& c) {
   L.ll = take(L.ll_words * 8);
   L.layer_tab = take((size_t)c.n_layers * sizeof(LayerPtrs<float>));
   L.trace = take((size_t)kMaxStepWG * (c.n_layers + 1) * 32 * 8);  // optional phase timestamps
-  L.nrm_cnt = take((size_t)(16384 / 64) * 4);
+  // One counter per 64-column block of a residual product.
+  L.nrm_ncnt = (int)(d / 64 + 1);
+  L.nrm_cnt = take((size_t)L.nrm_ncnt * 4);
   const size_t R = L.rows_cap, tm = bf ? 2 : 4;
   L.row_stream = take(R * 4);
   L.row_pos = take(R * 4);
@@ -203,7 +206,7 @@ Layout make_layout(const hh_config& c) {
   L.gemm_ws_bytes = std::min<size_t>((size_t)4 * R * std::max((size_t)2 * F, (size_t)L.nqkv) * 4, (size_t)256 << 20);
   L.gemm_ws = take(L.gemm_ws_bytes);
   L.scratch_u32 = take(256);
-  L.nrm_ss = take((size_t)32 * (16384 / 64) * 4);
+  L.nrm_ss = take((size_t)32 * (d / 64) * 4);
   L.total = off;
   return L;
 }
@@ -226,6 +229,7 @@ struct hh_ctx {
   hipStream_t stream = nullptr;
   bool loaded = false;
   bool use_graphs = true;
+  bool row_norm = true;  // HH_ROWNORM=0: every RMSNorm as a pass of its own (for comparison)
   float wscale = 1.f;  // MFMA weights hold w * wscale (fp16 repack); epilogues multiply by 1/wscale
   int step_wg = 0;     // workgroups of the persistent batch-1 decode kernel (0: not usable)
   bool step_q4 = false;  // the persistent kernel streams the stored 4-bit rows
@@ -300,9 +304,10 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
   // Lockstep decode rows on fp16 operands with tiled weights split each
   // RMSNorm across the residual product that feeds it and the product that
   // reads it (RowNorm); `pending`: h holds x * gain and the row sums of
-  // squares are in nrm_ss, not yet applied.
+  // squares are in nrm_ss, not yet applied.  (For prompt rows the large-tile
+  // kernels' arrival chain cost as much as the norm pass it replaced.)
   const bool rnorm = sizeof(TM) == 2 && !decode_gemv && prefill_stream < 0 && head_row == -1 &&
-                     !L.wqkvT16.empty() && GK::norm_fusable(d) && d / 64 <= 64;
+                     !L.wqkvT16.empty() && GK::norm_fusable(d) && d % 256 == 0 && d <= 2048 && c->row_norm;
   float* nss = rnorm ? c->at<float>(L.nrm_ss) : nullptr;
   int* ncnt = rnorm ? c->at<int>(L.nrm_cnt) : nullptr;
   RowNorm rn_use;
@@ -359,7 +364,8 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       }
       const TM* wo_t = tiled ? c->at<TM>(L.woT16[l]) : nullptr;
       if (fuse) {
-        pending = GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h, wo_t, nss, ncnt);
+        pending = GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, mn, eps, h, wo_t,
+                            nss, ncnt, L.nrm_ncnt);
       } else {
         GK::resid(st, gws, oM, n, c->at<TM>(L.woM[l]), hq * 64, d, ws, x, nullptr, 0.f, nullptr, wo_t);
         DK::rmsnorm_rows(st, n, x, mn, eps, d, h);
@@ -370,7 +376,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       // workgroups would each recompute the row factors.
       const float* next_an = (fuse && l + 1 < g.n_layers) ? c->at<float>(L.attn_norm[l + 1]) : nullptr;
       pending = GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h,
-                          tiled ? c->at<TM>(L.wdownT16[l]) : nullptr, next_an ? nss : nullptr, ncnt);
+                          tiled ? c->at<TM>(L.wdownT16[l]) : nullptr, next_an ? nss : nullptr, ncnt, L.nrm_ncnt);
     }
   }
   const float* fn = c->at<float>(L.final_norm);
@@ -873,6 +879,8 @@ hh_status hh_create(const hh_config* cfg, void* arena, size_t arena_bytes, void*
   if (const char* fw = std::getenv("HH_STEP_FAIL_WAIT")) c->step_fail_wait = std::atoi(fw) != 0;
   const char* ge = std::getenv("HH_GRAPHS");
   c->use_graphs = !(ge && ge[0] == '0');
+  const char* rne = std::getenv("HH_ROWNORM");
+  c->row_norm = !(rne && rne[0] == '0');
   c->len.assign(cfg->max_streams, 0);
   c->pages.assign(cfg->max_streams, {});
   for (int p = L.n_pages - 1; p >= 0; --p) c->free_pages.push_back(p);
