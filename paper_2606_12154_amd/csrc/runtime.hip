@@ -315,7 +315,7 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
   rn_use.nss = d / 64;
   rn_use.n = (float)d;
   rn_use.eps = eps;
-  bool pending = false;
+  bool pending = false, final_normed = false;
   for (int l = 0; l < g.n_layers; ++l) {
     const float* an = c->at<float>(L.attn_norm[l]);
     const float* mn = c->at<float>(L.mlp_norm[l]);
@@ -372,11 +372,14 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       }
       GK::gateup(st, gws, h, n, c->at<TM>(L.wguM[l]), d, F, ws, mM, tiled ? c->at<TM>(L.wguT16[l]) : nullptr,
                  pending ? rn_use : RowNorm());
-      // The final norm stays a pass of its own: the head's thousands of
-      // workgroups would each recompute the row factors.
-      const float* next_an = (fuse && l + 1 < g.n_layers) ? c->at<float>(L.attn_norm[l + 1]) : nullptr;
+      // The last layer's down projection takes the final norm along under
+      // RowNorm (the head reads h next).
+      const float* next_an = (fuse && l + 1 < g.n_layers) ? c->at<float>(L.attn_norm[l + 1])
+                             : (rnorm && l + 1 == g.n_layers) ? c->at<float>(L.final_norm)
+                                                              : nullptr;
       pending = GK::resid(st, gws, mM, n, c->at<TM>(L.wdownM[l]), F, d, ws, x, next_an, eps, h,
                           tiled ? c->at<TM>(L.wdownT16[l]) : nullptr, next_an ? nss : nullptr, ncnt, L.nrm_ncnt);
+      if (rnorm && l + 1 == g.n_layers) final_normed = true;
     }
   }
   const float* fn = c->at<float>(L.final_norm);
@@ -387,10 +390,12 @@ void enqueue_layers(hh_ctx* c, int n, bool decode_gemv, int s_max, int head_row,
       DK::head_gemv(st, c->at<TW>(L.lm_head), x, fn, eps, d, V, 0, rs, logits, slot);
     } else {
       TM* h = c->at<TM>(L.h);
-      if (GK::norm_fusable(d)) GK::rmsnorm(st, n, x, d, fn, eps, h);
-      else DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
+      if (!final_normed) {
+        if (GK::norm_fusable(d)) GK::rmsnorm(st, n, x, d, fn, eps, h);
+        else DK::rmsnorm_rows(st, n, x, fn, eps, d, h);
+      }
       GK::logits(st, gws, h, n, c->at<TM>(L.lm_headM), d, V, ws, logits, slot, rs,
-                 L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16));
+                 L.wqkvT16.empty() ? nullptr : c->at<TM>(L.lm_headT16), pending ? rn_use : RowNorm());
     }
   }
 }
