@@ -138,19 +138,21 @@ def test_multistream_lockstep(one_b, ctx):
     multistream_lockstep(model, shape, ctx, "1B 4-stream decode")
 
 
-def test_multistream_lockstep_batched_skinny(one_b):
-    """The same with the batched skinny kernel (HH_SKINNY_RES=0), which
-    serves grids or K ranges the resident one does not take; a context of its
-    own, run eagerly, so that no graph captured under the default is
-    replayed."""
+@pytest.mark.parametrize("env", [{"HH_SKINNY_RES": "0"}, {"HH_ROWNORM": "0"}], ids=["batched_skinny", "separate_norms"])
+def test_multistream_lockstep_variants(one_b, env):
+    """The same with the batched skinny kernel (HH_SKINNY_RES=0, which serves
+    grids or K ranges the resident one does not take, and norms as passes of
+    their own), and with the resident kernel but every RMSNorm as a pass of
+    its own (HH_ROWNORM=0); a context of its own, run eagerly, so that no
+    graph captured under the default is replayed."""
     shape, tensors, model = one_b
-    saved = {k: os.environ.get(k) for k in ("HH_SKINNY_RES", "HH_GRAPHS")}
-    os.environ["HH_SKINNY_RES"] = "0"
+    saved = {k: os.environ.get(k) for k in list(env) + ["HH_GRAPHS"]}
+    os.environ.update(env)
     os.environ["HH_GRAPHS"] = "0"
     c = None
     try:
         c = new_context(shape, tensors, streams=5, context=512, max_prefill=256)
-        multistream_lockstep(model, shape, c, "1B 4-stream decode, batched skinny kernel")
+        multistream_lockstep(model, shape, c, f"1B 4-stream decode, {env}")
     finally:
         if c is not None:
             c.close()
