@@ -499,7 +499,7 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
   // Folded QKV: this row's q heads g G .. g G + G - 1, then k and v of head
   // g (64 values each), and the new key and value as the cache stores them.
   __shared__ float qkv_s[(G + 2) * 64];
-  __shared__ TKV new_kv[2][64];
+  __shared__ __attribute__((aligned(16))) TKV new_kv[2][64];
   const int g = blockIdx.x, r = blockIdx.y;
   const bool folded = fold.part != nullptr;
   const int hkv = hq / G;
@@ -525,7 +525,10 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
     }
   }
   const int s = row_stream[r], p = row_pos[r], t = p + 1, npg = (t + kPage - 1) / kPage;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, key = lane >> 2, quarter = lane & 3;
+  // The wave index is uniform: taken into a scalar register, page choices and
+  // the last-page test below become scalar branches.
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63, key = lane >> 2,
+            quarter = lane & 3;
   const float qscale = 0.125f * 1.4426950408889634f;  // 1/sqrt(64) * log2(e)
   // Rotation of the pair (e, e + 32) this thread applies below (q heads and k).
   float2 cs = make_float2(1.f, 0.f);
@@ -617,35 +620,40 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
       for (int e = 0; e < 16; ++e) qv[h][e] = qkv_s[h * 64 + quarter * 16 + e] * qscale;
   }
 
+  // Softmax state per head: running max m (log2 units), sum and output.
   float m[G], lsum[G], o[G][16];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    m[h] = -INFINITY;
     lsum[h] = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[h][e] = 0.f;
   }
-  auto take = [&](const KvPage<TKV>& P, int pg) {
-    float kf[16], vf[16];
-#pragma unroll
-    for (int c = 0; c < (int)sizeof(TKV); ++c) {
-      widen16(P.k[c], kf + c * Vec16<TKV>::n, TKV());
-      widen16(P.v[c], vf + c * Vec16<TKV>::n, TKV());
-    }
+  // Only the row's last page holds keys past the stream's length (stale
+  // slots, possibly non-finite bit patterns: their V becomes 0, since
+  // 0 * NaN would be NaN, and their score -inf) and, with the QKV fold, the
+  // row's own key and value, which come from LDS (the cache write above may
+  // not be visible to this wave's loads yet).  Returns the lane's validity.
+  auto patch_last = [&](KvPage<TKV>& P, int pg) {
     const bool valid = pg * kPage + key < t;
-    // With the QKV fold the row's own key and value come from LDS (the
-    // cache write above may not be visible to this wave's loads yet).
     if (folded && pg * kPage + key == p) {
+      const u32x4* nk = reinterpret_cast<const u32x4*>(&new_kv[0][quarter * 16]);
+      const u32x4* nv = reinterpret_cast<const u32x4*>(&new_kv[1][quarter * 16]);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        kf[e] = (float)new_kv[0][quarter * 16 + e];
-        vf[e] = (float)new_kv[1][quarter * 16 + e];
+      for (int c = 0; c < (int)sizeof(TKV); ++c) {
+        P.k[c] = nk[c];
+        P.v[c] = nv[c];
       }
     }
-    // Slots past the stream's length hold stale data (possibly non-finite bit
-    // patterns): their weight is 0, and 0 * NaN would be NaN.
 #pragma unroll
-    for (int e = 0; e < 16; ++e) vf[e] = valid ? vf[e] : 0.f;
+    for (int c = 0; c < (int)sizeof(TKV); ++c) P.v[c] = valid ? P.v[c] : u32x4{0u, 0u, 0u, 0u};
+    return valid;
+  };
+  // Scores of the G heads for this lane's key (all four lanes of a key get
+  // the full dot product).
+  auto scores = [&](const KvPage<TKV>& P, float* sc) {
+    float kf[16];
+#pragma unroll
+    for (int c = 0; c < (int)sizeof(TKV); ++c) widen16(P.k[c], kf + c * Vec16<TKV>::n, TKV());
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       float a0 = 0.f, a1 = 0.f;
@@ -654,24 +662,72 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
         a0 = fmaf(qv[h][e], kf[e], a0);
         a1 = fmaf(qv[h][e + 1], kf[e + 1], a1);
       }
-      float sc = a0 + a1;
-      sc += dpp<0xB1>(sc);  // the 4 lanes of a key hold quarters of its dot product
-      sc += dpp<0x4E>(sc);
-      if (!valid) sc = -INFINITY;
-      const float mn = fmaxf(m[h], wave_max_u(sc));  // finite: every page has a valid key
-      const float alpha = exp2f(m[h] - mn);
-      const float pk = exp2f(sc - mn);
-      lsum[h] = lsum[h] * alpha + (quarter == 0 ? pk : 0.f);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[h][e] = fmaf(pk, vf[e], o[h][e] * alpha);
-      m[h] = mn;
+      float x = a0 + a1;
+      x += dpp<0xB1>(x);  // the 4 lanes of a key hold quarters of its dot product
+      x += dpp<0x4E>(x);
+      sc[h] = x;
     }
   };
+  // Weights exp2(score - m) into the sums; lsum runs on all four lanes of a
+  // key, so its total is taken a quarter below.
+  auto accumulate = [&](const KvPage<TKV>& P, const float* sc) {
+    float vf[16];
 #pragma unroll
-  for (int k = 0; k < PU; ++k)
-    if (wave + NW * k < npg) take(P[k], wave + NW * k);
-  // Longer rows: the next two pages' K/V are in flight while one is taken;
-  // loads past the end re-read the row's last page.
+    for (int c = 0; c < (int)sizeof(TKV); ++c) widen16(P.v[c], vf + c * Vec16<TKV>::n, TKV());
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float pk = __builtin_amdgcn_exp2f(sc[h] - m[h]);
+      lsum[h] += pk;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[h][e] = fmaf(pk, vf[e], o[h][e]);
+    }
+  };
+  // The wave's first PU pages are in registers together: scores of all of
+  // them first, one max per head over the wave, then the weighted sums (no
+  // rescaling).  Pages past the row's end (re-read copies) score -inf.
+  {
+    float sc[PU][G];
+#pragma unroll
+    for (int k = 0; k < PU; ++k) {
+      const int pg = wave + NW * k;
+      bool valid = pg < npg;
+      if (pg == npg - 1) valid = patch_last(P[k], pg);
+      scores(P[k], sc[k]);
+#pragma unroll
+      for (int h = 0; h < G; ++h) sc[k][h] = valid ? sc[k][h] : -INFINITY;
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float mx = sc[0][h];
+#pragma unroll
+      for (int k = 1; k < PU; ++k) mx = fmaxf(mx, sc[k][h]);
+      m[h] = wave_max_u(mx);  // -inf for a wave without pages
+    }
+#pragma unroll
+    for (int k = 0; k < PU; ++k)
+      if (wave + NW * k < npg) accumulate(P[k], sc[k]);
+  }
+  // Longer rows: later pages one at a time with an online update (the max
+  // is finite here: the wave took PU pages above); the next two pages' K/V
+  // are in flight while one is taken; loads past the end re-read the row's
+  // last page.
+  auto take = [&](KvPage<TKV>& P, int pg) {
+    bool valid = true;
+    if (pg == npg - 1) valid = patch_last(P, pg);
+    float sc[G];
+    scores(P, sc);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      sc[h] = valid ? sc[h] : -INFINITY;
+      const float mn = fmaxf(m[h], wave_max_u(sc[h]));
+      const float alpha = __builtin_amdgcn_exp2f(m[h] - mn);
+      lsum[h] *= alpha;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[h][e] *= alpha;
+      m[h] = mn;
+    }
+    accumulate(P, sc);
+  };
   if (long_row) __syncthreads();  // pts (the folded path's barriers came earlier)
   if (wave + NW * PU < npg) {
     KvPage<TKV>&A = P[0], &B = P[1], &C = P[2];
@@ -694,7 +750,7 @@ __global__ __launch_bounds__(512) void k_attn_rows(const float* __restrict__ q, 
   // the wave's slots; waves without pages leave m = -inf, l = 0, o = 0.
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float ls = wave_sum_u(lsum[h]);
+    const float ls = wave_sum_u(lsum[h]) * 0.25f;
     float* sw = st + ((wave * G + h) * 4 + (lane >> 4)) * SLOT;
     if ((lane & 15) == 0) {
       sw[0] = m[h];
