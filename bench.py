@@ -556,6 +556,12 @@ def main():
     ctx.close()
     del ctx
     torch.cuda.empty_cache()
+    if not args.no_other_configs:
+        # The same request on the 4-bit model (weights quantized at load).
+        q4 = measure_q4_decode(shape)
+        out.update({"q4_decode_tok_s": q4["decode_tok_s"], "q4_ms_per_token": q4["ms_per_token"],
+                    "q4_hbm_frac": q4["hbm_frac"], "q4_ttft_ms": q4["ttft_ms"]})
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res, cores = cpu_baseline(shape, wl["wseed"], prompt, args.cpu_decode_steps)
         (rate, pre_s), (rate32, pre32) = res["fp64"], res["fp32"]
