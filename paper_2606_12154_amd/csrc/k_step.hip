@@ -67,7 +67,7 @@ constexpr int kQ4ScaleOff = kQ4Rows * 1024;
 // wave gets some; the three sizes are the compiled variants of the row code.
 __host__ __device__ constexpr int q4_rows(int n) { return n <= 2 * kNC ? 2 : n <= 3 * kNC ? 3 : kQ4Rows; }
 constexpr int kMaxRing = 16;               // ring slots supported
-constexpr int kItemKvBytes = 64 * 1024;    // K/V bytes aimed at per attention item
+constexpr int kItemKvBytes = 32 * 1024;    // K/V bytes aimed at per attention item (swept: 16-64 KiB)
 constexpr int kMaxItemPages = 256;         // pages of one attention item
 constexpr int kMaxConsumerSplits = 2;      // splits per kv head merged by the O-phase consumers
 constexpr int kMaxGroup = 8;               // query heads per kv head (fp16 K/V)
