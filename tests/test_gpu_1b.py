@@ -94,23 +94,28 @@ def test_prefill_wide_tiles(one_b, ctx, prompt_ref, tile, n):
     assert nxt == int(np.argmax(got[-1]))
 
 
-def test_decode_teacher_forced(one_b, ctx):
+@pytest.mark.parametrize("plen,steps", [(256, 40), (140, 6), (100, 4)], ids=["p256", "p140", "p100"])
+def test_decode_teacher_forced(one_b, ctx, plen, steps):
+    """The batch-1 kernel against the oracle.  With attention items of at
+    most 8 pages: 256 + 40 positions take three splits per kv head (combined
+    at the producer), 140 + 6 two (combined by the O-phase consumers) and
+    100 + 4 one."""
     shape, _, model = one_b
-    prompt = synth.make_tokens(shape.vocab, 256, 2)
+    prompt = synth.make_tokens(shape.vocab, plen, 2)
     ref_last, cache = model.prefill(prompt, rows="last")
     ctx.reset()
     nxt, last = ctx.prefill(0, prompt, logits="last")
     worst = check_logits(last, ref_last[0], TOL, what="prefill last")
     tok = int(np.argmax(ref_last[0]))
-    # 40 steps: attended lengths 257 .. 296 include item lengths that are
-    # whole 32-key slots (t = 272, 288), where the step's own key and value
-    # sit in the last row of a streamed slot.
-    for i in range(40):
+    # With 256 + 40: attended lengths 257 .. 296 include item lengths that
+    # are whole 32-key slots (t = 272, 288), where the step's own key and
+    # value sit in the last row of a streamed slot.
+    for i in range(steps):
         ref = model.decode(cache, tok)
         _, lg = ctx.decode_step([0], [tok], logits=True)
         worst = max(worst, check_logits(lg[0], ref, TOL, what=f"decode step {i}"))
         tok = int(np.argmax(ref))
-    print(f"1B teacher-forced decode: max-abs {worst:.4g}")
+    print(f"1B teacher-forced decode ({plen} + {steps}): max-abs {worst:.4g}")
 
 
 def multistream_lockstep(model, shape, ctx, what):
