@@ -168,6 +168,30 @@ def test_multistream_lockstep_variants(one_b, env):
                 os.environ[k] = v
 
 
+def test_multistream_long_row(one_b):
+    """A stream longer than the 32 pages (512 positions) the fp16 row
+    attention keeps in registers up front, decoded in lockstep with a short
+    one: the online loop over its later pages against the oracle."""
+    shape, tensors, model = one_b
+    c = None
+    try:
+        c = new_context(shape, tensors, streams=2, context=600, max_prefill=256)
+        lens = [530, 20]
+        prompts = [synth.make_tokens(shape.vocab, n, 600 + i) for i, n in enumerate(lens)]
+        caches = []
+        for i, p in enumerate(prompts):
+            c.prefill(i, p)
+            caches.append(model.prefill(p, rows="last")[1])
+        feed = np.array([17, 29], dtype=np.int32)
+        _, lg = c.decode_step([0, 1], feed, logits=True)
+        worst = max(check_logits(lg[k], model.decode(caches[k], int(feed[k])), TOL, what=f"long row {k}")
+                    for k in range(2))
+        print(f"1B lockstep with a 531-position row: max-abs {worst:.4g}")
+    finally:
+        if c is not None:
+            c.close()
+
+
 @pytest.fixture(scope="module")
 def forced_256(one_b):
     """The bench prompt (256 tokens, seed 2) and 8 teacher-forced steps of the

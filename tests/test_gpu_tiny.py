@@ -160,6 +160,38 @@ def test_prefill_batch_matches_oracle(tiny):
     assert ctx.length(1) == 0 and ctx.length(4) == 0
 
 
+def test_long_rows_lockstep_and_batch(tiny):
+    """Rows longer than the pages the row attention keeps in registers up
+    front (three per wave for an fp32 cache: 24 pages, 384 positions) take
+    its online page loop: a 450-token stream decoded in lockstep with a short
+    one, and a 420-token prompt in a batch prefill (rows past 384 attend
+    with the same loop), against the oracle run of each stream alone."""
+    shape, tensors, model = tiny
+    ctx = new_context(shape, tensors, streams=3, context=640)
+    try:
+        lens = [450, 20]
+        prompts = [synth.make_tokens(shape.vocab, n, 500 + i) for i, n in enumerate(lens)]
+        caches = []
+        for i, p in enumerate(prompts):
+            ctx.prefill(i, p)
+            caches.append(model.prefill(p, rows="last")[1])
+        rng = np.random.default_rng(9)
+        for step in range(3):
+            feed = rng.integers(0, shape.vocab, size=2).astype(np.int32)
+            _, lg = ctx.decode_step([0, 1], feed, logits=True)
+            for k in range(2):
+                check_logits(lg[k], model.decode(caches[k], int(feed[k])), TOL, what=f"long rows step {step} row {k}")
+        long_prompt = synth.make_tokens(shape.vocab, 420, 510)
+        nxt = ctx.prefill_batch([2], [long_prompt])
+        ref, cache2 = model.prefill(long_prompt, rows="last")
+        if top2_margin(ref[0]) > 1e-2:
+            assert int(nxt[0]) == int(np.argmax(ref[0]))
+        _, lg = ctx.decode_step([2], [7], logits=True)
+        check_logits(lg[0], model.decode(cache2, 7), TOL, what="after a 420-token batch prefill")
+    finally:
+        ctx.close()
+
+
 def test_chunked_and_appended_prefill(tiny):
     shape, tensors, model = tiny
     toks = synth.make_tokens(shape.vocab, 70, 3)
