@@ -69,3 +69,28 @@ def test_g8_chunked_prefill_and_lockstep(g8):
     finally:
         ctx.close()
     print(f"G8 chunked prefill + 3-stream lockstep: max-abs {worst:.4g}")
+
+
+def test_g8_lockstep_long_row(g8):
+    """A 400-token stream (25 pages: past the three pages per wave the
+    eight-head row attention holds in registers up front) decoded in
+    lockstep with a short one."""
+    tensors, model = g8
+    lens = [400, 30]
+    prompts = [synth.make_tokens(G8.vocab, n, 90 + i) for i, n in enumerate(lens)]
+    ctx = new_context(G8, tensors, streams=2, context=480, max_prefill=128)
+    try:
+        caches = []
+        for s, p in enumerate(prompts):
+            ctx.prefill(s, p)
+            caches.append(model.prefill(p, rows="last")[1])
+        rng = np.random.default_rng(10)
+        worst = 0.0
+        for step in range(2):
+            feed = rng.integers(0, G8.vocab, size=2).astype(np.int32)
+            _, lg = ctx.decode_step([0, 1], feed, logits=True)
+            ref = model.decode_batch(caches, feed)
+            worst = max(worst, check_logits(lg, ref, TOL, what=f"G8 long-row step {step}"))
+    finally:
+        ctx.close()
+    print(f"G8 lockstep with a 401-position row: max-abs {worst:.4g}")
