@@ -410,10 +410,14 @@ __device__ __forceinline__ void make_plan(Plan& pl, const StepParams<TW, TKV>& P
   constexpr int pps = kSlot / page_bytes;                          // pages per ring slot
   const int npg = (t + kPage - 1) / kPage;
   // Items of kItemKvBytes while that makes at most 16 splits per kv head;
-  // longer caches take items twice that size (more splits cost more in the
-  // producer's combine than the shorter items save: 4,096 cached positions
-  // 1,429 against 1,412 tok/s).
-  const int cap = (npg <= 16 * (kItemKvBytes / page_bytes) ? kItemKvBytes : 2 * kItemKvBytes) / page_bytes;
+  // longer caches keep about 16 splits with items of up to four times that
+  // size, and beyond that as many splits as there are workgroups per kv
+  // head.  Measured, tok/s at 2,048 / 8,192 / 16,384 cached positions:
+  // 1,505 / 1,360 / 1,305; 1,499 / 1,351 / 1,305 with 64 KiB items past 16
+  // splits; 1,507 / 1,371 / 1,225 with 16 splits at every length (too few
+  // workgroups streaming the longest caches).
+  int cap = kItemKvBytes / page_bytes;
+  if (npg > 16 * cap) cap = min((npg + 15) / 16, 4 * cap);
   const int s_cap = nwg / hkv;
   int nspl = (npg + cap - 1) / cap;
   nspl = nspl < s_cap ? nspl : s_cap;
