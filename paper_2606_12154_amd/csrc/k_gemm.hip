@@ -1326,6 +1326,11 @@ static WideCfg wide_choice(GemmKind kind, int M, int n_cols, int K) {
   // 3.34 ms against the small-tile kernel, which stays better at 256 rows;
   // eight waves 29.3 -> 28.1 us.
   if (kind == GemmKind::QKV && M >= 512) return WideCfg{128, 128, 1, 8};
+  // QKV at 256 .. 511 rows: the same tiles with a 4-way K split (192
+  // workgroups; the split-K reduction applies the epilogue): TTFT at 256
+  // rows 1.68-1.69 -> 1.64 ms against the small-tile kernel's 3-way split
+  // (2-, 3- and 6-way splits, four waves and 128 x 256 tiles all slower).
+  if (kind == GemmKind::QKV && M >= 256) return WideCfg{128, 128, 4, 8};
   return WideCfg{0, 0, 1, 4};
 }
 
