@@ -1085,8 +1085,8 @@ __global__ __launch_bounds__(256 * KW) void k_gemm_skinny(const _Float16* __rest
 }
 
 // Activation-resident variant, for grids of at most two workgroups per CU:
-// every wave issues all of its weight loads at once (at most 32 K blocks, 32
-// KiB per wave), the workgroup's activation range (32 rows x at most 1024 K
+// every wave issues its first weight loads with the activations and the rest
+// (at most 32 K blocks, 32 KiB per wave, in all) once those have landed, the workgroup's activation range (32 rows x at most 1024 K
 // per K group) goes into LDS once, and each block's MFMAs wait only for that
 // block's weights.  The batched kernel above pays an L2 round trip and a
 // barrier per 256 K of activations, and keeps two batches in flight: at 32
@@ -1142,16 +1142,24 @@ __global__ __launch_bounds__(256 * KW) void k_gemm_skinny_res(const _Float16* __
       xv[i][q] = __builtin_bit_cast(f16x8, __builtin_amdgcn_raw_buffer_load_b128(xres, off, 0, 0));
     }
   // The scheduler would otherwise start the LDS stores (and so wait for the
-  // activations) before issuing most of the weight loads.
+  // activations) before issuing the first weight loads.
   __builtin_amdgcn_sched_barrier(0);
   // Wave (rb, kg) starts its tiles at block `rot` of its range and wraps
   // around, so that the waves' first requests do not all fall on 32 KiB
   // boundaries (every range starts on one).
   const int rot = nkb > 0 ? (rb * 13 + kg * 7) % nkb : 0;
   auto blk = [&](int u) { return u + rot < nkb ? u + rot : u + rot - nkb; };
+  // Only the first W0 weight blocks go out with the activations: with every
+  // block issued at once, the activations (a shared 128 KiB per workgroup,
+  // from memory after the producing launch) came back behind the weight
+  // stream, ~10 us into a 13.5 us gate/up launch, and every MFMA waited for
+  // them.  The rest of the weights follow once the activations have landed
+  // (the 32-row step 0.957 -> 0.947 ms; 4, 12 and 16 blocks first measured
+  // 0.948, 0.951 and 0.954).
+  constexpr int W0 = NB < 8 ? NB : 8;
   f16x8 w[NB];
 #pragma unroll
-  for (int u = 0; u < NB; ++u)
+  for (int u = 0; u < W0; ++u)
     w[u] = __builtin_bit_cast(
         f16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, u < nkb ? wvoff + 1024u * blk(u) : kOob, 0, kNt));
   __builtin_amdgcn_sched_barrier(0);
@@ -1163,6 +1171,12 @@ __global__ __launch_bounds__(256 * KW) void k_gemm_skinny_res(const _Float16* __
       _Float16* dst = kc < 4 * nkb ? xs + (rw + 4 * i) * pitch + 8 * kc : sink;
       *reinterpret_cast<f16x8*>(dst) = xv[i][q];
     }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int u = W0; u < NB; ++u)
+    w[u] = __builtin_bit_cast(
+        f16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, u < nkb ? wvoff + 1024u * blk(u) : kOob, 0, kNt));
+  __builtin_amdgcn_sched_barrier(0);
   __syncthreads();
 
   f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
